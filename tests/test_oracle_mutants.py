@@ -1,0 +1,52 @@
+"""Plant plausible mistakes in copies of the oracle and check that the pins
+in test_oracle.py catch every one (CPU only; the real oracle is untouched)."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+SRC = os.path.join(ROOT, "oracle", "oracle.cpp")
+
+# (name, exact text in oracle.cpp, replacement)
+MUTANTS = [
+    ("bias_dropped", "        acc += b[n];\n        s += std::fabs(b[n]);\n      }\n      Y[m * N + n] = acc;",
+     "        s += std::fabs(b[n]);\n      }\n      Y[m * N + n] = acc;"),
+    ("fwd_weight_transposed", "        double p = X[m * K + k] * W[n * K + k];\n        acc += p;\n        s += std::fabs(p);\n      }\n      if (b) {\n        acc += b[n];\n        s += std::fabs(b[n]);\n      }\n      Y[m * N + n]",
+     "        double p = X[m * K + k] * W[k * N + n];\n        acc += p;\n        s += std::fabs(p);\n      }\n      if (b) {\n        acc += b[n];\n        s += std::fabs(b[n]);\n      }\n      Y[m * N + n]"),
+    ("dx_sign_flipped", "        double p = g * W[n * K + k];\n        acc[k] += p;",
+     "        double p = g * W[n * K + k];\n        acc[k] -= p;"),
+    ("dw_upstream_index_swapped", "      double g = dY[m * N + n];\n      for (int64_t k = 0; k < K; ++k) {\n        double p = g * X[m * K + k];",
+     "      double g = dY[(m % N) * N + (n % M)];\n      for (int64_t k = 0; k < K; ++k) {\n        double p = g * X[m * K + k];"),
+    ("db_off_by_one_row", "    for (int64_t m = 0; m < M; ++m) {\n      acc += dY[m * N + n];",
+     "    for (int64_t m = 1; m < M; ++m) {\n      acc += dY[m * N + n];"),
+    ("S_without_abs", "        acc += p;\n        s += std::fabs(p);\n      }\n      if (b) {",
+     "        acc += p;\n        s += p;\n      }\n      if (b) {"),
+    ("broadcast_batch_not_clamped",
+     "  for (int i = 0; i < p.nbatch; ++i) off = off * opbatch[i] + (opbatch[i] == 1 ? 0 : idx[i]);",
+     "  for (int i = 0; i < p.nbatch; ++i) off = off * opbatch[i] + (opbatch[i] == 1 ? 0 : idx[i] % 2);"),
+    ("grad_skips_broadcast_sum", "        for (int64_t bi = 0; bi < nbatch; ++bi) {\n          if (amap[bi] != ai) continue;",
+     "        for (int64_t bi = 0; bi < nbatch; ++bi) {\n          if (amap[bi] != ai || bi != amap[bi] * (nbatch / (nabatch ? nabatch : 1))) continue;"),
+    ("reduce_keeps_wrong_axis", "    for (int d = 0; d < nout_dims; ++d) j = j * pin[d] + (pin[d] == 1 ? 0 : idx[d]);",
+     "    for (int d = 0; d < nout_dims; ++d) j = j * pin[d] + (pin[d] == 1 ? 0 : idx[d] % pin[d]);\n    if (nout_dims > 1 && pin[0] == 1) continue;"),
+    ("broadcast_rule_accepts_mismatch", "    else return OR_ERR_SHAPE;\n    out[n - 1 - i] = d;",
+     "    else d = da > db ? da : db;\n    out[n - 1 - i] = d;"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_mutant(tmp_path, name, old, new):
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} not unique/found"
+    mutated = tmp_path / "oracle_mut.cpp"
+    mutated.write_text(src.replace(old, new))
+    lib = tmp_path / "liboracle_mut.so"
+    subprocess.run(["g++", "-std=c++17", "-O1", "-fopenmp", "-ffp-contract=off", "-fPIC", "-shared",
+                    "-o", str(lib), str(mutated)], check=True)
+    env = dict(os.environ, MT_ORACLE_LIB_OVERRIDE=str(lib), OMP_NUM_THREADS="2")
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(HERE, "test_oracle.py")], cwd=ROOT, env=env,
+                       capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"mutant {name} survived the oracle pins:\n{r.stdout[-2000:]}"
