@@ -1,0 +1,208 @@
+#!/usr/bin/env python3
+"""Throughput of the dense-layer training step on one MI355X.
+
+One step = the whole hot path on one batch of synthetic inputs already in
+HBM: Y = X W^T + b (mt_linear_fwd), then dX = dY W, dW = dY^T X and
+db = 1^T dY (mt_linear_bwd, issued one output at a time so that HIP events
+bracket each kernel; the kernels are the ones a single call with all three
+outputs launches, in the same order, on the same stream).
+
+Prints ONE JSON line: TFLOP/s of the three products (6 M N K flop per step)
+over the timed steps, the dominant kernel's roofline, and the fp64 CPU
+oracle timed on a bounded sample as a baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix peak (256 CU x 256 flop/clk x 2.4 GHz)
+BF16_MFMA_PEAK_TFLOPS = 2516.6  # MI355X dense bf16 matrix peak
+HBM_PEAK_GBS = 8000.0
+METRIC = "TFLOP/s for linear fwd+bwd (3 GEMMs) at M=N=K=8192 fp32; % MFMA peak"
+
+# sources whose text decides the measured kernels (for staleness of counters)
+KERNEL_SOURCES = ["paper_2602_00125_amd/csrc/gemm_f32.hip", "paper_2602_00125_amd/csrc/reduce.hip",
+                  "paper_2602_00125_amd/csrc/gemm_bf16.hip", "paper_2602_00125_amd/csrc/capi.cpp"]
+
+
+def sources_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        p = os.path.join(ROOT, rel)
+        if os.path.exists(p):
+            h.update(rel.encode())
+            h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="linear_8192x8192x8192_f32")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target wall time of the CPU-oracle baseline sample (0 disables it)")
+    return ap.parse_args()
+
+
+def cpu_baseline(inp, seconds: float):
+    """Time the fp64 oracle on a bounded random sample of the step's outputs."""
+    import numpy as np
+
+    import oracle
+
+    X = inp["X"].double().numpy() if inp["X"].dtype != __import__("torch").bfloat16 else None
+    if X is None:
+        to64 = lambda t: oracle.bf16_bits_to_f64(t.view(__import__("torch").int16).numpy())
+        X, W, dY = to64(inp["X"]), to64(inp["W"]), to64(inp["dY"])
+    else:
+        W, dY = inp["W"].double().numpy(), inp["dY"].double().numpy()
+    B = inp["b"].double().numpy()
+    M, K = X.shape
+    N = W.shape[0]
+    rng = np.random.default_rng(0)
+    macs = 0
+    done = 0
+    t0 = time.perf_counter()
+    chunk = 64
+    while True:
+        r, c = rng.integers(0, M, chunk), rng.integers(0, N, chunk)
+        oracle.linear_fwd_at(X, W, B, r, c)
+        r, c = rng.integers(0, M, chunk), rng.integers(0, K, chunk)
+        oracle.linear_bwd_dx_at(dY, W, r, c)
+        r, c = rng.integers(0, N, chunk), rng.integers(0, K, chunk)
+        oracle.linear_bwd_dw_at(dY, X, r, c)
+        macs += chunk * (K + N + M)
+        done += chunk
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+        if el < seconds / 8:
+            chunk *= 2
+    el = time.perf_counter() - t0
+    return {"value": 2.0 * macs / el / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"{done} random output elements of each of Y, dX, dW (full-length fp64 dot "
+                      f"products with the |a*b| bound) in {el:.1f} s; TFLOP/s = 2*MACs/s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "
+              f"multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2602_00125_amd import binding as mt
+    from paper_2602_00125_amd import workloads as wl
+
+    w = wl.WORKLOADS[args.workload]
+    assert isinstance(w, wl.LinearWorkload), "the bench times the dense-layer step"
+    dev = torch.device("cuda:0")
+    inp = w.make()
+    x, wt, bias, dy = (inp[k].to(dev) for k in ("X", "W", "b", "dY"))
+    M, N, K = w.M, w.N, w.K
+    y = torch.empty(M, N, device=dev)
+    dx = torch.empty(M, K, device=dev)
+    dw = torch.empty(N, K, device=dev)
+    db = torch.empty(N, device=dev)
+    ws_bytes = mt.linear_bwd_workspace(x, wt, dy, dx, dw, db)
+    ws = torch.empty(max(ws_bytes, 256) // 4 + 64, device=dev) if ws_bytes else None
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        mt.linear_fwd(x, wt, bias, y)
+        if ev is not None:
+            ev[1].record()
+        mt.linear_bwd(x, wt, dy, dx, None, None, workspace=ws)
+        if ev is not None:
+            ev[2].record()
+        mt.linear_bwd(x, wt, dy, None, dw, None, workspace=ws)
+        if ev is not None:
+            ev[3].record()
+        mt.linear_bwd(x, wt, dy, None, None, db, workspace=ws)
+        if ev is not None:
+            ev[4].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    for i in range(args.steps):
+        step(events[i])
+    t_end.record()
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    per = {"fwd_nt_gemm": 0.0, "dx_nn_gemm": 0.0, "dw_tn_gemm": 0.0, "db_colsum": 0.0}
+    for ev in events:
+        for j, k in enumerate(per):
+            per[k] += ev[j].elapsed_time(ev[j + 1])
+    per = {k: v / args.steps for k, v in per.items()}
+    ms_per_step = total_ms / args.steps
+    flops = w.flops()
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    gemm_flops = 2.0 * M * N * K
+    is_bf16 = w.dtype == "bf16"
+    peak = BF16_MFMA_PEAK_TFLOPS if is_bf16 else FP32_MFMA_PEAK_TFLOPS
+    dominant = max(("fwd_nt_gemm", "dx_nn_gemm", "dw_tn_gemm"), key=lambda k: per[k])
+    achieved = gemm_flops / (per[dominant] * 1e-3) / 1e12
+    # HBM traffic of the dominant kernel from committed rocprofv3 counters, if
+    # they were taken on the current kernel sources
+    traffic = None
+    tfile = os.path.join(ROOT, "profiles", "traffic.json")
+    if os.path.exists(tfile):
+        try:
+            rec = json.load(open(tfile)).get(args.workload, {}).get(dominant)
+            if rec and rec.get("sources_hash") == sources_hash():
+                traffic = rec["hbm_bytes_per_launch"]
+        except (ValueError, OSError):
+            traffic = None
+    db_bytes = M * N * (2 if is_bf16 else 4) + N * 4
+    out = {
+        "metric": METRIC if args.workload == "linear_8192x8192x8192_f32" else
+        f"TFLOP/s for linear fwd+bwd (3 GEMMs) on {args.workload}",
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if is_bf16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "M": M, "N": N, "K": K,
+                   "inputs": "seeded synthetic, resident in HBM before timing",
+                   "pct_of_mfma_peak": round(100.0 * value / peak, 2)},
+        "roofline": {"bound": "mfma", "kernel": dominant, "achieved": round(achieved, 3),
+                     "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                     "traffic": traffic},
+        "kernels_ms": {k: round(v, 4) for k, v in per.items()},
+        "db_colsum_gbs": round(db_bytes / (per["db_colsum"] * 1e-3) / 1e9, 1),
+    }
+    if args.cpu_seconds > 0:
+        out["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

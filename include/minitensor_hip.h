@@ -1,0 +1,174 @@
+/*
+ * libminitensor_hip: MI355X (gfx950) kernels for the dense layer and the
+ * broadcasting matmul of MiniTensor, with their reverse-mode gradients.
+ *
+ * Operations (MiniTensor paper):
+ *   Sec. 3.1, Eq. (1)   matmul Y = X W^T, and the NumPy/PyTorch broadcasting
+ *                       rule (left-pad with singleton dims, virtually expand
+ *                       size-1 dims without materialising them).
+ *   Sec. 3.2, Eq. (4)   matmul pullbacks  Xbar += Ybar W,  Wbar += Ybar^T X;
+ *                       add pullback      xbar += zbar (summed over the axes
+ *                       an input was broadcast along).
+ *   Sec. 3.3, Eq. (5)   Dense(x; W, b) = x W^T + 1 b^T.
+ *   Sec. 3.5            gradient buffers exist only when a backward needs them
+ *                       (here: a null output pointer skips its work).
+ *
+ * Conventions for every entry point
+ *   - Tensors are described by mt_tensor: a device pointer, a dtype, a rank
+ *     and per-dim sizes and strides counted in ELEMENTS (not bytes).
+ *   - The caller owns every buffer. No entry point allocates device memory.
+ *     Workspace, where an entry point takes one, is caller-supplied device
+ *     memory; its required size comes from the matching *_workspace call.
+ *     A NULL workspace (or one that is too small) selects a slower variant
+ *     that needs none, so workspace only ever buys speed.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     All device work is enqueued on it asynchronously; results are visible
+ *     after the caller synchronises that stream.
+ *   - Every argument is validated on the host before any HIP call. On failure
+ *     the call returns a non-zero mt_status, enqueues nothing, leaves every
+ *     output untouched and records a message for mt_last_error() (per
+ *     thread). A failed launch returns MT_ERR_HIP with HIP's error string.
+ *     Device faults surface at the caller's next synchronisation. No C++
+ *     exception or abort crosses this interface.
+ *   - Outputs must not overlap any input or each other (MT_ERR_ALIAS).
+ *   - Results are deterministic: no floating-point atomics are used, so the
+ *     same call on the same inputs returns bit-identical outputs.
+ *   - Floating point: fp32 operands are multiplied and accumulated in fp32
+ *     (matrix cores, v_mfma_f32_32x32x2_f32). bf16 operands are multiplied
+ *     exactly and accumulated in fp32 (v_mfma_f32_32x32x16_bf16). Every
+ *     output, bias and bias gradient is fp32.
+ */
+#ifndef MINITENSOR_HIP_H
+#define MINITENSOR_HIP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MT_MAX_DIMS 8
+
+typedef enum { MT_F32 = 0, MT_BF16 = 1 } mt_dtype;
+
+typedef enum {
+  MT_OK = 0,
+  MT_ERR_NULL = 1,        /* a required pointer is NULL */
+  MT_ERR_NDIM = 2,        /* rank outside what the operation accepts */
+  MT_ERR_SHAPE = 3,       /* sizes do not match / do not broadcast */
+  MT_ERR_DTYPE = 4,       /* unsupported dtype or dtype combination */
+  MT_ERR_LAYOUT = 5,      /* strides the kernels cannot address */
+  MT_ERR_ALIAS = 6,       /* an output overlaps an input or another output */
+  MT_ERR_WORKSPACE = 7,   /* workspace pointer given with a bad size/alignment */
+  MT_ERR_HIP = 8,         /* the HIP runtime reported an error */
+  MT_ERR_INVALID = 9      /* any other invalid argument (flags, negative size) */
+} mt_status;
+
+/* A strided view of device memory. Sizes and strides are in elements. */
+typedef struct {
+  void* data;
+  int32_t dtype;                 /* mt_dtype */
+  int32_t ndim;                  /* 0..MT_MAX_DIMS */
+  int64_t shape[MT_MAX_DIMS];
+  int64_t stride[MT_MAX_DIMS];
+} mt_tensor;
+
+/* Flags. */
+#define MT_ACCUMULATE 1u   /* out += result (the "+=" of the pullbacks, Sec. 3.2);
+                              default: out = result */
+#define MT_REDUCE_INTO 2u  /* mt_matmul: c may have the shape of the full result
+                              summed over some batch axes (the un-broadcast shape
+                              of an operand); the sum is folded into the product */
+
+/* ------------------------------------------------------------------ linear
+ * mt_linear_fwd: Y = X W^T + 1 b^T (Eq. (5); with b == NULL, Eq. (1)).
+ *   x [M, K]  f32 or bf16          w [N, K] same dtype as x
+ *   b [N]     f32, or NULL          y [M, N] f32
+ * Matrix operands may have any row pitch (stride[0] >= inner size) but their
+ * inner dim must be contiguous (stride[1] == 1; MT_ERR_LAYOUT otherwise).
+ * b must be contiguous. M, N or K may be 0 (K == 0 writes y = b or 0).
+ */
+mt_status mt_linear_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* b,
+                        const mt_tensor* y, void* stream);
+
+/* mt_linear_bwd: gradients of Eq. (5) from the upstream gradient dY:
+ *   dx [M, K] = dY W        (Eq. (4))       f32, or NULL to skip
+ *   dw [N, K] = dY^T X      (Eq. (4))       f32, or NULL to skip
+ *   db [N]    = 1^T dY      (add pullback)  f32, or NULL to skip
+ *   x [M, K], w [N, K], dy [M, N] share one dtype (f32 or bf16); x may be
+ *   NULL when dw is NULL and w may be NULL when dx is NULL.
+ * flags: MT_ACCUMULATE adds into dx/dw/db instead of overwriting.
+ * ws/ws_bytes: optional workspace (size from mt_linear_bwd_workspace); used
+ * for split reductions of db and split-K partial sums of dw.
+ */
+mt_status mt_linear_bwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* dy,
+                        const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db,
+                        uint32_t flags, void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes mt_linear_bwd can use for these arguments (0 if none). */
+mt_status mt_linear_bwd_workspace(const mt_tensor* x, const mt_tensor* w, const mt_tensor* dy,
+                                  const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db,
+                                  size_t* bytes);
+
+/* -------------------------------------------------------------- matmul
+ * mt_matmul: C = A @ B with NumPy/PyTorch matmul semantics (Eq. (1) per
+ * batch element, batch dims broadcast per Sec. 3.1):
+ *   - a and b have rank >= 1; a 1-D a is treated as [1, K] and a 1-D b as
+ *     [K, 1], the added dim being dropped from the result;
+ *   - the batch dims (all but the last two) broadcast; a broadcast dim may
+ *     have any stride (including 0);
+ *   - the two matrix dims of each operand must have one of them contiguous:
+ *     stride[-1] == 1 (row-major) or stride[-2] == 1 (a transposed view);
+ *   - a and b share one dtype (f32 or bf16); c is f32, row-major contiguous,
+ *     with exactly the result shape, or, with MT_REDUCE_INTO, that shape
+ *     summed over some batch axes (leading axes dropped, kept axes of size
+ *     1), i.e. the gradient of a broadcast operand.
+ * flags: MT_ACCUMULATE, MT_REDUCE_INTO. ws is reserved (pass NULL/0).
+ */
+mt_status mt_matmul(const mt_tensor* a, const mt_tensor* b, const mt_tensor* c, uint32_t flags,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/* mt_reduce_broadcast_grad: the add pullback through a broadcast (Sec. 3.1,
+ * Sec. 3.2): grad_in = grad_out summed over every axis along which an input
+ * of grad_in's shape was broadcast to grad_out's shape. grad_in's shape,
+ * left-padded with ones, must equal grad_out's shape except for dims of
+ * size 1. grad_out: f32, any strides. grad_in: f32, row-major contiguous.
+ * flags: MT_ACCUMULATE. ws: optional (mt_reduce_broadcast_grad_workspace).
+ */
+mt_status mt_reduce_broadcast_grad(const mt_tensor* grad_out, const mt_tensor* grad_in,
+                                   uint32_t flags, void* ws, size_t ws_bytes, void* stream);
+
+mt_status mt_reduce_broadcast_grad_workspace(const mt_tensor* grad_out, const mt_tensor* grad_in,
+                                             size_t* bytes);
+
+/* ------------------------------------------------- host-only shape helpers
+ * No GPU needed; results are exact. Shapes are arrays of int64 sizes.
+ * mt_broadcast_shape: the broadcast of two shapes (Sec. 3.1).
+ * mt_matmul_shape:    the result shape of mt_matmul for operand shapes a, b.
+ * *nout receives the rank, out[] (room for MT_MAX_DIMS) the sizes.
+ */
+mt_status mt_broadcast_shape(int32_t na, const int64_t* a, int32_t nb, const int64_t* b,
+                             int32_t* nout, int64_t* out);
+mt_status mt_matmul_shape(int32_t na, const int64_t* a, int32_t nb, const int64_t* b,
+                          int32_t* nout, int64_t* out);
+
+/* Testing and tuning knobs (process-wide, not thread-safe; 0 = accepted,
+ * -1 = unknown key). Keys: "cfg" GEMM tile configuration (-1 = automatic,
+ * 0 = 256x256, 1 = 256x128, 2 = 128x256, 3 = 128x128, 4 = 64x64);
+ * "vec1" (1 = force the 4-byte-load kernels); "splits" (split-K count for
+ * mt_linear_bwd's dw, 0 = automatic); "parts" (row slices of the db and
+ * broadcast-gradient reductions, 0 = automatic). Results stay within the
+ * documented accuracy for every setting. */
+int mt_debug_set(const char* key, int64_t value);
+
+/* Static description of a status code. */
+const char* mt_status_str(mt_status s);
+/* Message describing this thread's last failed call ("" if none). */
+const char* mt_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MINITENSOR_HIP_H */

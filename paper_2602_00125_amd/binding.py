@@ -1,0 +1,193 @@
+"""ctypes binding of libminitensor_hip (argument marshalling only).
+
+Every function here builds ``mt_tensor`` descriptors from torch tensors
+(device memory owned by torch) and calls the C entry point of the same name
+on the current HIP stream; all arithmetic runs in the library's HIP kernels.
+Importing this module raises ImportError when the library has not been built
+(``python paper_2602_00125_amd/build.py``): there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libminitensor_hip.so")
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run `python paper_2602_00125_amd/build.py`")
+lib = ctypes.CDLL(LIB_PATH)
+
+MAX_DIMS = 8
+F32, BF16 = 0, 1
+ACCUMULATE, REDUCE_INTO = 1, 2
+STATUS = {0: "MT_OK", 1: "MT_ERR_NULL", 2: "MT_ERR_NDIM", 3: "MT_ERR_SHAPE", 4: "MT_ERR_DTYPE",
+          5: "MT_ERR_LAYOUT", 6: "MT_ERR_ALIAS", 7: "MT_ERR_WORKSPACE", 8: "MT_ERR_HIP",
+          9: "MT_ERR_INVALID"}
+
+EXPORTS = ["mt_linear_fwd", "mt_linear_bwd", "mt_linear_bwd_workspace", "mt_matmul",
+           "mt_reduce_broadcast_grad", "mt_reduce_broadcast_grad_workspace", "mt_broadcast_shape",
+           "mt_matmul_shape", "mt_debug_set", "mt_status_str", "mt_last_error"]
+
+
+class MtTensor(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32), ("ndim", ctypes.c_int32),
+                ("shape", ctypes.c_int64 * MAX_DIMS), ("stride", ctypes.c_int64 * MAX_DIMS)]
+
+
+_P = ctypes.POINTER(MtTensor)
+_vp, _sz, _u32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_uint32
+_I64P = ctypes.POINTER(ctypes.c_int64)
+lib.mt_linear_fwd.argtypes = [_P, _P, _P, _P, _vp]
+lib.mt_linear_bwd.argtypes = [_P, _P, _P, _P, _P, _P, _u32, _vp, _sz, _vp]
+lib.mt_linear_bwd_workspace.argtypes = [_P, _P, _P, _P, _P, _P, ctypes.POINTER(_sz)]
+lib.mt_matmul.argtypes = [_P, _P, _P, _u32, _vp, _sz, _vp]
+lib.mt_reduce_broadcast_grad.argtypes = [_P, _P, _u32, _vp, _sz, _vp]
+lib.mt_reduce_broadcast_grad_workspace.argtypes = [_P, _P, ctypes.POINTER(_sz)]
+lib.mt_broadcast_shape.argtypes = [ctypes.c_int32, _I64P, ctypes.c_int32, _I64P,
+                                   ctypes.POINTER(ctypes.c_int32), _I64P]
+lib.mt_matmul_shape.argtypes = lib.mt_broadcast_shape.argtypes
+lib.mt_debug_set.argtypes = [ctypes.c_char_p, ctypes.c_int64]
+lib.mt_status_str.argtypes = [ctypes.c_int]
+lib.mt_status_str.restype = ctypes.c_char_p
+lib.mt_last_error.argtypes = []
+lib.mt_last_error.restype = ctypes.c_char_p
+for _f in ("mt_linear_fwd", "mt_linear_bwd", "mt_linear_bwd_workspace", "mt_matmul",
+           "mt_reduce_broadcast_grad", "mt_reduce_broadcast_grad_workspace", "mt_broadcast_shape",
+           "mt_matmul_shape", "mt_debug_set"):
+    getattr(lib, _f).restype = ctypes.c_int
+
+
+class MtError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        self.name = STATUS.get(status, str(status))
+        msg = lib.mt_last_error().decode()
+        super().__init__(f"{where}: {self.name}: {msg}")
+
+
+def _check(status: int, where: str) -> None:
+    if status != 0:
+        raise MtError(status, where)
+
+
+def raw_desc(ptr: int, dtype: int, shape, stride) -> MtTensor:
+    """A descriptor from raw values (tests of the host-side validation)."""
+    d = MtTensor()
+    d.data = ptr
+    d.dtype = dtype
+    d.ndim = len(shape)
+    for i, (s, st) in enumerate(zip(shape, stride)):
+        d.shape[i] = int(s)
+        d.stride[i] = int(st)
+    return d
+
+
+def desc(t: torch.Tensor | None):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("libminitensor_hip works on device tensors (got a CPU tensor)")
+    if t.dtype == torch.float32:
+        dt = F32
+    elif t.dtype == torch.bfloat16:
+        dt = BF16
+    else:
+        raise TypeError(f"unsupported dtype {t.dtype}")
+    if t.dim() > MAX_DIMS:
+        raise ValueError(f"rank {t.dim()} > {MAX_DIMS}")
+    return raw_desc(t.data_ptr(), dt, t.shape, t.stride())
+
+
+def _ref(d):
+    return None if d is None else ctypes.byref(d)
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _ws(workspace):
+    if workspace is None:
+        return None, 0
+    assert workspace.is_cuda
+    return workspace.data_ptr(), workspace.numel() * workspace.element_size()
+
+
+def linear_fwd(x, w, b, y, stream=None) -> None:
+    """y = x w^T + b on the device (b may be None)."""
+    dx_, dw_, db_, dy_ = desc(x), desc(w), desc(b), desc(y)
+    _check(lib.mt_linear_fwd(_ref(dx_), _ref(dw_), _ref(db_), _ref(dy_), _stream(stream)),
+           "mt_linear_fwd")
+
+
+def linear_bwd_workspace(x, w, dy, dx=None, dw=None, db=None) -> int:
+    n = _sz(0)
+    ds = [desc(t) for t in (x, w, dy, dx, dw, db)]
+    _check(lib.mt_linear_bwd_workspace(*[_ref(d) for d in ds], ctypes.byref(n)),
+           "mt_linear_bwd_workspace")
+    return int(n.value)
+
+
+def linear_bwd(x, w, dy, dx=None, dw=None, db=None, accumulate=False, workspace=None,
+               stream=None) -> None:
+    """dx = dy w, dw = dy^T x, db = column sums of dy (None skips an output)."""
+    ds = [desc(t) for t in (x, w, dy, dx, dw, db)]
+    ptr, nbytes = _ws(workspace)
+    _check(lib.mt_linear_bwd(*[_ref(d) for d in ds], ACCUMULATE if accumulate else 0, ptr, nbytes,
+                             _stream(stream)), "mt_linear_bwd")
+
+
+def matmul(a, b, c, accumulate=False, reduce_into=False, stream=None) -> None:
+    """c = a @ b with broadcasting (c summed over broadcast axes with reduce_into)."""
+    flags = (ACCUMULATE if accumulate else 0) | (REDUCE_INTO if reduce_into else 0)
+    da, db_, dc = desc(a), desc(b), desc(c)
+    _check(lib.mt_matmul(_ref(da), _ref(db_), _ref(dc), flags, None, 0, _stream(stream)),
+           "mt_matmul")
+
+
+def reduce_broadcast_grad_workspace(grad_out, grad_in) -> int:
+    n = _sz(0)
+    _check(lib.mt_reduce_broadcast_grad_workspace(_ref(desc(grad_out)), _ref(desc(grad_in)),
+                                                  ctypes.byref(n)),
+           "mt_reduce_broadcast_grad_workspace")
+    return int(n.value)
+
+
+def reduce_broadcast_grad(grad_out, grad_in, accumulate=False, workspace=None, stream=None) -> None:
+    """grad_in = grad_out summed over the axes grad_in was broadcast along."""
+    ptr, nbytes = _ws(workspace)
+    _check(lib.mt_reduce_broadcast_grad(_ref(desc(grad_out)), _ref(desc(grad_in)),
+                                        ACCUMULATE if accumulate else 0, ptr, nbytes,
+                                        _stream(stream)), "mt_reduce_broadcast_grad")
+
+
+def _shape_call(fn, a, b, where):
+    aa = (ctypes.c_int64 * max(1, len(a)))(*a)
+    bb = (ctypes.c_int64 * max(1, len(b)))(*b)
+    out = (ctypes.c_int64 * MAX_DIMS)()
+    n = ctypes.c_int32(0)
+    _check(fn(len(a), aa, len(b), bb, ctypes.byref(n), out), where)
+    return tuple(out[i] for i in range(n.value))
+
+
+def broadcast_shape(a, b) -> tuple:
+    return _shape_call(lib.mt_broadcast_shape, tuple(a), tuple(b), "mt_broadcast_shape")
+
+
+def matmul_shape(a, b) -> tuple:
+    return _shape_call(lib.mt_matmul_shape, tuple(a), tuple(b), "mt_matmul_shape")
+
+
+def debug_set(key: str, value: int) -> None:
+    if lib.mt_debug_set(key.encode(), int(value)) != 0:
+        raise KeyError(key)
+
+
+def status_str(code: int) -> str:
+    return lib.mt_status_str(code).decode()

@@ -1,0 +1,594 @@
+// C-ABI of libminitensor_hip: argument validation, shape planning and kernel
+// dispatch. Declarations and their contracts: include/minitensor_hip.h.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+
+#include "../../include/minitensor_hip.h"
+#include "gemm_params.hpp"
+#include "kernels.hpp"
+#include "shape.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+// Knobs for tests and tuning (mt_debug_set): -1 / 0 = automatic.
+int g_force_cfg = -1;
+int g_force_vec1 = 0;
+int g_force_splits = 0;
+int g_force_parts = 0;
+
+mt_status fail(mt_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+size_t elem_size(int32_t dt) { return dt == MT_BF16 ? 2 : 4; }
+
+mt_status check_tensor(const mt_tensor* t, const char* name, int min_nd, int max_nd) {
+  if (!t) return fail(MT_ERR_NULL, std::string(name) + ": null tensor descriptor");
+  if (t->ndim < min_nd || t->ndim > max_nd)
+    return fail(MT_ERR_NDIM, std::string(name) + ": rank " + std::to_string(t->ndim) +
+                                 " outside " + std::to_string(min_nd) + ".." +
+                                 std::to_string(max_nd));
+  if (t->dtype != MT_F32 && t->dtype != MT_BF16)
+    return fail(MT_ERR_DTYPE, std::string(name) + ": unknown dtype " + std::to_string(t->dtype));
+  int64_t n = 1;
+  for (int i = 0; i < t->ndim; ++i) {
+    if (t->shape[i] < 0) return fail(MT_ERR_SHAPE, std::string(name) + ": negative size");
+    if (t->stride[i] < 0) return fail(MT_ERR_LAYOUT, std::string(name) + ": negative stride");
+    n *= t->shape[i];
+  }
+  if (n > 0 && !t->data) return fail(MT_ERR_NULL, std::string(name) + ": null data pointer");
+  return MT_OK;
+}
+
+int64_t numel(const mt_tensor* t) {
+  int64_t n = 1;
+  for (int i = 0; i < t->ndim; ++i) n *= t->shape[i];
+  return n;
+}
+
+// [lo, hi) byte range touched by a view; empty views touch nothing.
+void byte_range(const mt_tensor* t, uintptr_t* lo, uintptr_t* hi) {
+  const int64_t span = mt::span_elems(t->ndim, t->shape, t->stride);
+  *lo = (uintptr_t)t->data;
+  *hi = *lo + (uintptr_t)span * elem_size(t->dtype);
+}
+
+bool overlaps(const mt_tensor* a, const mt_tensor* b) {
+  if (!a || !b || numel(a) == 0 || numel(b) == 0) return false;
+  uintptr_t alo, ahi, blo, bhi;
+  byte_range(a, &alo, &ahi);
+  byte_range(b, &blo, &bhi);
+  return alo < bhi && blo < ahi;
+}
+
+bool is_row_major(const mt_tensor* t) {
+  int64_t expect = 1;
+  for (int i = t->ndim - 1; i >= 0; --i) {
+    if (t->shape[i] != 1 && t->stride[i] != expect) return false;
+    expect *= t->shape[i];
+  }
+  return true;
+}
+
+mt_status hip_status(hipError_t e) {
+  if (e == hipSuccess) return MT_OK;
+  return fail(MT_ERR_HIP, std::string("HIP: ") + hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+int choose_cfg(int64_t M, int64_t N, int64_t batch) {
+  if (g_force_cfg >= 0) return g_force_cfg;
+  auto tiles = [&](int64_t bm, int64_t bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn) * batch; };
+  if (tiles(256, 256) >= 512) return mt::kCfg256x256;
+  if (tiles(256, 128) >= 512) return mt::kCfg256x128;
+  if (tiles(128, 128) >= 128) return mt::kCfg128x128;
+  return mt::kCfg64x64;
+}
+
+// Split-K count for an un-batched product whose tile grid under-fills the chip.
+int choose_splits(int64_t M, int64_t N, int64_t K, int cfg) {
+  if (g_force_splits > 0) return g_force_splits;
+  const int64_t tiles = ((M + mt::gemm_tile_m(cfg) - 1) / mt::gemm_tile_m(cfg)) *
+                        ((N + mt::gemm_tile_n(cfg) - 1) / mt::gemm_tile_n(cfg));
+  if (tiles >= 192) return 1;
+  int64_t s = 256 / (tiles > 0 ? tiles : 1);
+  const int64_t kmax = K / 512;  // keep at least 512 of K per slice
+  if (s > kmax) s = kmax;
+  if (s > 16) s = 16;
+  return s < 1 ? 1 : (int)s;
+}
+
+void init_params(mt::GemmParams* p) {
+  std::memset(p, 0, sizeof(*p));
+  p->keep_count = 1;
+  p->red_count = 1;
+  p->group_m = 4;
+  p->splits = 1;
+}
+
+struct GemmCall {
+  mt::GemmParams p;
+  bool a_kc, b_kc;
+  bool vec4;
+  int cfg;
+};
+
+// Everything the fp32 kernels need checked for 16-byte vector access.
+bool vec4_ok_operand(const void* base, bool kc, int64_t rows_other, int64_t contig_extent,
+                     int64_t ld, const int64_t* bstrides, int nb) {
+  if (!aligned16(base) || contig_extent % 4 != 0) return false;
+  if (rows_other > 1 && ld % 4 != 0) return false;
+  for (int i = 0; i < nb; ++i)
+    if (bstrides[i] % 4 != 0) return false;
+  (void)kc;
+  return true;
+}
+
+mt_status launch_gemm(GemmCall& g, hipStream_t stream, void* ws, size_t ws_bytes) {
+  mt::GemmParams& p = g.p;
+  if (p.M == 0 || p.N == 0 || p.keep_count == 0) return MT_OK;
+  if (g.cfg < 0) g.cfg = choose_cfg(p.M, p.N, p.keep_count);
+  if (g_force_vec1) g.vec4 = false;
+  // the 4-byte-load kernels keep their staging registers within budget up to 128x128
+  if (!g.vec4 && (g.cfg == mt::kCfg256x256 || g.cfg == mt::kCfg256x128 || g.cfg == mt::kCfg128x256))
+    g.cfg = mt::kCfg128x128;
+  // 32-bit buffer offsets: one tile's rows times the row pitch must stay below 2 GiB
+  const int64_t rows_a = g.a_kc ? mt::gemm_tile_m(g.cfg) : mt::gemm_tile_k(g.cfg);
+  const int64_t rows_b = g.b_kc ? mt::gemm_tile_n(g.cfg) : mt::gemm_tile_k(g.cfg);
+  if (rows_a * p.lda * 4 >= (int64_t)1 << 31 || rows_b * p.ldb * 4 >= (int64_t)1 << 31)
+    return fail(MT_ERR_LAYOUT, "row pitch too large for 32-bit tile offsets");
+  p.splits = 1;
+  p.k_per_split = p.K > 0 ? p.K : 1;
+  if (ws && p.keep_count == 1 && p.red_count == 1) {
+    const int s = choose_splits(p.M, p.N, p.K, g.cfg);
+    const int64_t bk = mt::gemm_tile_k(g.cfg);
+    if (s > 1) {
+      const int64_t kps = ((p.K + s - 1) / s + bk - 1) / bk * bk;
+      const int splits = (int)((p.K + kps - 1) / kps);
+      const size_t need = (size_t)splits * p.M * p.N * sizeof(float);
+      if (splits > 1 && need <= ws_bytes) {
+        p.splits = splits;
+        p.k_per_split = kps;
+        p.partial = (float*)ws;
+        p.partial_stride = p.M * p.N;
+      }
+    }
+  }
+  (void)hipGetLastError();  // clear a stale error so the launch check is ours
+  hipError_t e = mt::gemm_f32(p, g.a_kc, g.b_kc, g.vec4, g.cfg, stream);
+  if (e != hipSuccess) return hip_status(e);
+  if (p.splits > 1) {
+    e = mt::splitk_finish(p.partial, p.splits, p.M, p.N, p.c, p.ldc, p.bias, p.accumulate != 0,
+                          stream);
+    if (e != hipSuccess) return hip_status(e);
+  }
+  return MT_OK;
+}
+
+mt_status check_matrix(const mt_tensor* t, const char* name) {
+  mt_status s = check_tensor(t, name, 2, 2);
+  if (s) return s;
+  if (t->shape[1] > 1 && t->stride[1] != 1)
+    return fail(MT_ERR_LAYOUT, std::string(name) + ": inner dim must be contiguous (stride 1)");
+  return MT_OK;
+}
+
+int64_t pitch(const mt_tensor* t) {
+  return t->shape[0] > 1 ? t->stride[0] : (t->shape[1] > 0 ? t->shape[1] : 1);
+}
+
+mt_status check_out_matrix(const mt_tensor* t, const char* name) {
+  mt_status s = check_matrix(t, name);
+  if (s) return s;
+  if (t->dtype != MT_F32) return fail(MT_ERR_DTYPE, std::string(name) + ": outputs are f32");
+  if (t->shape[0] > 1 && t->stride[0] < t->shape[1])
+    return fail(MT_ERR_LAYOUT, std::string(name) + ": rows overlap (row pitch < columns)");
+  return MT_OK;
+}
+
+mt_status check_vector(const mt_tensor* t, const char* name, int64_t n) {
+  mt_status s = check_tensor(t, name, 1, 1);
+  if (s) return s;
+  if (t->dtype != MT_F32) return fail(MT_ERR_DTYPE, std::string(name) + ": must be f32");
+  if (t->shape[0] != n)
+    return fail(MT_ERR_SHAPE, std::string(name) + ": length " + std::to_string(t->shape[0]) +
+                                  ", expected " + std::to_string(n));
+  if (n > 1 && t->stride[0] != 1) return fail(MT_ERR_LAYOUT, std::string(name) + ": must be contiguous");
+  return MT_OK;
+}
+
+mt_status linear_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor* dy,
+                          const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db,
+                          uint32_t flags, void* ws, size_t ws_bytes, hipStream_t stream,
+                          size_t* ws_query) {
+  if (flags & ~MT_ACCUMULATE) return fail(MT_ERR_INVALID, "mt_linear_bwd: unknown flags");
+  mt_status s = check_matrix(dy, "dy");
+  if (s) return s;
+  const int64_t M = dy->shape[0], N = dy->shape[1];
+  const int32_t dt = dy->dtype;
+  int64_t K = -1;
+  if (dw) {
+    if ((s = check_matrix(x, "x"))) return s;
+    if (x->dtype != dt) return fail(MT_ERR_DTYPE, "x and dy must share a dtype");
+    if (x->shape[0] != M) return fail(MT_ERR_SHAPE, "x rows must equal dy rows");
+    K = x->shape[1];
+  }
+  if (dx) {
+    if ((s = check_matrix(w, "w"))) return s;
+    if (w->dtype != dt) return fail(MT_ERR_DTYPE, "w and dy must share a dtype");
+    if (w->shape[0] != N) return fail(MT_ERR_SHAPE, "w rows must equal dy columns");
+    if (K >= 0 && w->shape[1] != K) return fail(MT_ERR_SHAPE, "w and x disagree on K");
+    K = w->shape[1];
+  }
+  if (dx) {
+    if ((s = check_out_matrix(dx, "dx"))) return s;
+    if (dx->shape[0] != M || dx->shape[1] != K) return fail(MT_ERR_SHAPE, "dx must be [M, K]");
+  }
+  if (dw) {
+    if ((s = check_out_matrix(dw, "dw"))) return s;
+    if (dw->shape[0] != N || dw->shape[1] != K) return fail(MT_ERR_SHAPE, "dw must be [N, K]");
+  }
+  if (db && (s = check_vector(db, "db", N))) return s;
+  if (dt == MT_BF16) return fail(MT_ERR_DTYPE, "bf16 operands are not supported yet");
+  // inputs actually read: dy always, x for dw, w for dx
+  const mt_tensor* ins[3] = {dy, dw ? x : nullptr, dx ? w : nullptr};
+  const mt_tensor* outs[3] = {dx, dw, db};
+  for (int i = 0; i < 3; ++i) {
+    if (!outs[i]) continue;
+    for (int j = 0; j < 3; ++j)
+      if (overlaps(outs[i], ins[j])) return fail(MT_ERR_ALIAS, "an output overlaps an input");
+    for (int j = i + 1; j < 3; ++j)
+      if (overlaps(outs[i], outs[j])) return fail(MT_ERR_ALIAS, "outputs overlap");
+  }
+  const bool acc = (flags & MT_ACCUMULATE) != 0;
+
+  // workspace needs: dw split-K partials and db row-slice sums (used in turn)
+  size_t need_dw = 0, need_db = 0;
+  GemmCall gdw{};
+  if (dw && N > 0 && K > 0) {
+    init_params(&gdw.p);
+    gdw.p.a = dy->data;
+    gdw.p.b = x->data;
+    gdw.p.c = (float*)dw->data;
+    gdw.p.M = N;
+    gdw.p.N = K;
+    gdw.p.K = M;
+    gdw.p.lda = pitch(dy);
+    gdw.p.ldb = pitch(x);
+    gdw.p.ldc = pitch(dw);
+    gdw.p.accumulate = acc;
+    gdw.a_kc = false;
+    gdw.b_kc = false;
+    gdw.vec4 = vec4_ok_operand(dy->data, false, M, N, gdw.p.lda, nullptr, 0) &&
+               vec4_ok_operand(x->data, false, M, K, gdw.p.ldb, nullptr, 0) &&
+               aligned16(dw->data) && K % 4 == 0 && gdw.p.ldc % 4 == 0;
+    gdw.cfg = choose_cfg(N, K, 1);
+    const int sp = choose_splits(N, K, M, gdw.cfg);
+    if (sp > 1) need_dw = (size_t)sp * N * K * sizeof(float);
+  }
+  int parts = 1;
+  if (db && N > 0) {
+    parts = g_force_parts > 0 ? g_force_parts : mt::colsum_parts(M, N);
+    if (parts > 1) need_db = (size_t)parts * N * sizeof(float);
+  }
+  if (ws_query) {
+    *ws_query = need_dw > need_db ? need_dw : need_db;
+    return MT_OK;
+  }
+  if (ws && ((uintptr_t)ws & 255))
+    return fail(MT_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+
+  if (dx && M > 0 && K > 0) {
+    GemmCall g{};
+    init_params(&g.p);
+    g.p.a = dy->data;
+    g.p.b = w->data;
+    g.p.c = (float*)dx->data;
+    g.p.M = M;
+    g.p.N = K;
+    g.p.K = N;
+    g.p.lda = pitch(dy);
+    g.p.ldb = pitch(w);
+    g.p.ldc = pitch(dx);
+    g.p.accumulate = acc;
+    g.a_kc = true;
+    g.b_kc = false;
+    g.vec4 = vec4_ok_operand(dy->data, true, M, N, g.p.lda, nullptr, 0) &&
+             vec4_ok_operand(w->data, false, N, K, g.p.ldb, nullptr, 0) && aligned16(dx->data) &&
+             K % 4 == 0 && g.p.ldc % 4 == 0;
+    g.cfg = -1;
+    if ((s = launch_gemm(g, stream, nullptr, 0))) return s;
+  }
+  if (dw && N > 0 && K > 0) {
+    if ((s = launch_gemm(gdw, stream, ws, ws && ws_bytes >= need_dw ? ws_bytes : 0))) return s;
+  }
+  if (db && N > 0) {
+    (void)hipGetLastError();
+    float* wsp = (ws && parts > 1 && ws_bytes >= need_db) ? (float*)ws : nullptr;
+    hipError_t e = mt::colsum(dy->data, dt == MT_BF16, M, N, pitch(dy), (float*)db->data, acc,
+                              wsp, parts, stream);
+    if (e != hipSuccess) return hip_status(e);
+  }
+  return MT_OK;
+}
+
+mt_status matmul_impl(const mt_tensor* a, const mt_tensor* b, const mt_tensor* c, uint32_t flags,
+                      hipStream_t stream) {
+  if (flags & ~(MT_ACCUMULATE | MT_REDUCE_INTO)) return fail(MT_ERR_INVALID, "mt_matmul: unknown flags");
+  mt_status s;
+  if ((s = check_tensor(a, "a", 1, MT_MAX_DIMS))) return s;
+  if ((s = check_tensor(b, "b", 1, MT_MAX_DIMS))) return s;
+  if ((s = check_tensor(c, "c", 0, MT_MAX_DIMS))) return s;
+  if (a->dtype != b->dtype) return fail(MT_ERR_DTYPE, "a and b must share a dtype");
+  if (c->dtype != MT_F32) return fail(MT_ERR_DTYPE, "c must be f32");
+  if (a->dtype == MT_BF16) return fail(MT_ERR_DTYPE, "bf16 operands are not supported yet");
+  mt::MatmulPlan pl;
+  std::string err;
+  if ((s = mt::plan_matmul_shapes(a->ndim, a->shape, a->stride, b->ndim, b->shape, b->stride, &pl,
+                                  &err)))
+    return fail(s, "mt_matmul: " + err);
+  if (!is_row_major(c)) return fail(MT_ERR_LAYOUT, "c must be row-major contiguous");
+  // match c against the result shape (exact, or summed over batch dims)
+  const int nmat = pl.nout - pl.nbatch;  // result dims after the batch dims (0..2)
+  if (c->ndim < nmat || c->ndim > pl.nout) return fail(MT_ERR_SHAPE, "c has the wrong rank");
+  for (int i = 0; i < nmat; ++i)
+    if (c->shape[c->ndim - nmat + i] != pl.out[pl.nbatch + i])
+      return fail(MT_ERR_SHAPE, "c matrix dims do not match the product");
+  const bool reduce_into = (flags & MT_REDUCE_INTO) != 0;
+  const int cb = c->ndim - nmat;  // c batch rank
+  if (!reduce_into && cb != pl.nbatch) return fail(MT_ERR_SHAPE, "c has the wrong rank (no MT_REDUCE_INTO)");
+  mt::GemmParams p;
+  init_params(&p);
+  int64_t c_batch_stride[MT_MAX_DIMS];
+  {
+    int64_t st = 1;
+    for (int i = c->ndim - 1; i >= 0; --i) {
+      if (i < cb) c_batch_stride[i] = st;
+      st *= c->shape[i];
+    }
+  }
+  for (int d = 0; d < pl.nbatch; ++d) {
+    const int ci = d - (pl.nbatch - cb);
+    const int64_t cd = ci >= 0 ? c->shape[ci] : 1;
+    if (cd == pl.batch[d]) {
+      if (cd == 1) continue;
+      p.keep_shape[p.nkeep] = cd;
+      p.keep_sa[p.nkeep] = pl.sa[d];
+      p.keep_sb[p.nkeep] = pl.sb[d];
+      p.keep_sc[p.nkeep] = c_batch_stride[ci];
+      ++p.nkeep;
+    } else if (cd == 1 && reduce_into) {
+      p.red_shape[p.nred] = pl.batch[d];
+      p.red_sa[p.nred] = pl.sa[d];
+      p.red_sb[p.nred] = pl.sb[d];
+      ++p.nred;
+    } else {
+      return fail(MT_ERR_SHAPE, "c batch dims do not match the product");
+    }
+  }
+  if (overlaps(c, a) || overlaps(c, b)) return fail(MT_ERR_ALIAS, "c overlaps an input");
+  for (int i = 0; i < p.nkeep; ++i) p.keep_count *= p.keep_shape[i];
+  for (int i = 0; i < p.nred; ++i) p.red_count *= p.red_shape[i];
+  if (pl.M == 0 || pl.N == 0 || p.keep_count == 0) return MT_OK;
+  GemmCall g{};
+  g.p = p;
+  bool a_kc, b_kc;
+  int64_t lda, ldb;
+  if (!mt::operand_layout(pl.a, true, &a_kc, &lda))
+    return fail(MT_ERR_LAYOUT, "a: neither matrix dim is contiguous");
+  if (!mt::operand_layout(pl.b, false, &b_kc, &ldb))
+    return fail(MT_ERR_LAYOUT, "b: neither matrix dim is contiguous");
+  g.p.a = a->data;
+  g.p.b = b->data;
+  g.p.c = (float*)c->data;
+  g.p.M = pl.M;
+  g.p.N = pl.N;
+  g.p.K = pl.K;
+  g.p.lda = lda;
+  g.p.ldb = ldb;
+  g.p.ldc = pl.N;
+  g.p.accumulate = (flags & MT_ACCUMULATE) != 0;
+  if (p.red_count == 0) g.p.K = 0;  // an empty summed batch contributes nothing
+  g.a_kc = a_kc;
+  g.b_kc = b_kc;
+  int64_t sa_all[2 * MT_MAX_DIMS], sb_all[2 * MT_MAX_DIMS];
+  int na = 0;
+  for (int i = 0; i < p.nkeep; ++i) { sa_all[na] = p.keep_sa[i]; sb_all[na++] = p.keep_sb[i]; }
+  for (int i = 0; i < p.nred; ++i) { sa_all[na] = p.red_sa[i]; sb_all[na++] = p.red_sb[i]; }
+  g.vec4 = vec4_ok_operand(a->data, a_kc, a_kc ? pl.M : pl.K, a_kc ? pl.K : pl.M, lda, sa_all, na) &&
+           vec4_ok_operand(b->data, b_kc, b_kc ? pl.N : pl.K, b_kc ? pl.K : pl.N, ldb, sb_all, na) &&
+           aligned16(c->data) && pl.N % 4 == 0;
+  g.cfg = -1;
+  return launch_gemm(g, stream, nullptr, 0);
+}
+
+mt_status reduce_impl(const mt_tensor* go, const mt_tensor* gi, uint32_t flags, void* ws,
+                      size_t ws_bytes, hipStream_t stream, size_t* ws_query) {
+  if (flags & ~MT_ACCUMULATE) return fail(MT_ERR_INVALID, "mt_reduce_broadcast_grad: unknown flags");
+  mt_status s;
+  if ((s = check_tensor(go, "grad_out", 0, MT_MAX_DIMS))) return s;
+  if ((s = check_tensor(gi, "grad_in", 0, MT_MAX_DIMS))) return s;
+  if (go->dtype != MT_F32 || gi->dtype != MT_F32)
+    return fail(MT_ERR_DTYPE, "grad_out and grad_in must be f32");
+  if (!is_row_major(gi)) return fail(MT_ERR_LAYOUT, "grad_in must be row-major contiguous");
+  mt::ReducePlan plan;
+  std::string err;
+  if ((s = mt::plan_reduce(go->ndim, go->shape, go->stride, gi->ndim, gi->shape, &plan, &err)))
+    return fail(s, "mt_reduce_broadcast_grad: " + err);
+  const int parts = g_force_parts > 0 ? g_force_parts : mt::reduce_parts(plan);
+  const size_t need = parts > 1 ? (size_t)parts * plan.keep_count * sizeof(float) : 0;
+  if (ws_query) {
+    *ws_query = need;
+    return MT_OK;
+  }
+  if (overlaps(go, gi)) return fail(MT_ERR_ALIAS, "grad_in overlaps grad_out");
+  if (ws && ((uintptr_t)ws & 255)) return fail(MT_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  (void)hipGetLastError();
+  float* wsp = (ws && need && ws_bytes >= need) ? (float*)ws : nullptr;
+  return hip_status(mt::reduce_strided((const float*)go->data, plan, (float*)gi->data,
+                                       (flags & MT_ACCUMULATE) != 0, wsp, wsp ? parts : 1, stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+mt_status mt_linear_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* b,
+                        const mt_tensor* y, void* stream) {
+  try {
+    mt_status s;
+    if ((s = check_matrix(x, "x")) || (s = check_matrix(w, "w")) ||
+        (s = check_out_matrix(y, "y")))
+      return s;
+    if (x->dtype != w->dtype) return fail(MT_ERR_DTYPE, "x and w must share a dtype");
+    const int64_t M = x->shape[0], K = x->shape[1], N = w->shape[0];
+    if (w->shape[1] != K) return fail(MT_ERR_SHAPE, "w must be [N, K] with x [M, K]");
+    if (y->shape[0] != M || y->shape[1] != N) return fail(MT_ERR_SHAPE, "y must be [M, N]");
+    if (b && (s = check_vector(b, "b", N))) return s;
+    if (x->dtype == MT_BF16) return fail(MT_ERR_DTYPE, "bf16 operands are not supported yet");
+    if (overlaps(y, x) || overlaps(y, w) || overlaps(y, b))
+      return fail(MT_ERR_ALIAS, "y overlaps an input");
+    if (M == 0 || N == 0) return MT_OK;
+    GemmCall g{};
+    init_params(&g.p);
+    g.p.a = x->data;
+    g.p.b = w->data;
+    g.p.c = (float*)y->data;
+    g.p.bias = (b && N > 0) ? (const float*)b->data : nullptr;
+    g.p.M = M;
+    g.p.N = N;
+    g.p.K = K;
+    g.p.lda = pitch(x);
+    g.p.ldb = pitch(w);
+    g.p.ldc = pitch(y);
+    g.a_kc = true;
+    g.b_kc = true;
+    g.vec4 = vec4_ok_operand(x->data, true, M, K, g.p.lda, nullptr, 0) &&
+             vec4_ok_operand(w->data, true, N, K, g.p.ldb, nullptr, 0) && aligned16(y->data) &&
+             N % 4 == 0 && g.p.ldc % 4 == 0 && (!g.p.bias || aligned16(g.p.bias));
+    g.cfg = -1;
+    return launch_gemm(g, (hipStream_t)stream, nullptr, 0);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_linear_bwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* dy,
+                        const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db,
+                        uint32_t flags, void* ws, size_t ws_bytes, void* stream) {
+  try {
+    return linear_bwd_impl(x, w, dy, dx, dw, db, flags, ws, ws_bytes, (hipStream_t)stream, nullptr);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_linear_bwd_workspace(const mt_tensor* x, const mt_tensor* w, const mt_tensor* dy,
+                                  const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db,
+                                  size_t* bytes) {
+  try {
+    if (!bytes) return fail(MT_ERR_NULL, "bytes is null");
+    return linear_bwd_impl(x, w, dy, dx, dw, db, 0, nullptr, 0, nullptr, bytes);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_matmul(const mt_tensor* a, const mt_tensor* b, const mt_tensor* c, uint32_t flags,
+                    void* ws, size_t ws_bytes, void* stream) {
+  try {
+    (void)ws;
+    (void)ws_bytes;
+    return matmul_impl(a, b, c, flags, (hipStream_t)stream);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_reduce_broadcast_grad(const mt_tensor* grad_out, const mt_tensor* grad_in,
+                                   uint32_t flags, void* ws, size_t ws_bytes, void* stream) {
+  try {
+    return reduce_impl(grad_out, grad_in, flags, ws, ws_bytes, (hipStream_t)stream, nullptr);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_reduce_broadcast_grad_workspace(const mt_tensor* grad_out, const mt_tensor* grad_in,
+                                             size_t* bytes) {
+  try {
+    if (!bytes) return fail(MT_ERR_NULL, "bytes is null");
+    return reduce_impl(grad_out, grad_in, 0, nullptr, 0, nullptr, bytes);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_broadcast_shape(int32_t na, const int64_t* a, int32_t nb, const int64_t* b,
+                             int32_t* nout, int64_t* out) {
+  try {
+    if (!nout || !out) return fail(MT_ERR_NULL, "null output");
+    std::string err;
+    int n = 0;
+    mt_status s = mt::broadcast_shapes(na, a, nb, b, &n, out, &err);
+    if (s) return fail(s, err);
+    *nout = n;
+    return MT_OK;
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_matmul_shape(int32_t na, const int64_t* a, int32_t nb, const int64_t* b,
+                          int32_t* nout, int64_t* out) {
+  try {
+    if (!nout || !out || (na > 0 && !a) || (nb > 0 && !b)) return fail(MT_ERR_NULL, "null pointer");
+    mt::MatmulPlan pl;
+    std::string err;
+    mt_status s = mt::plan_matmul_shapes(na, a, nullptr, nb, b, nullptr, &pl, &err);
+    if (s) return fail(s, err);
+    *nout = pl.nout;
+    for (int i = 0; i < pl.nout; ++i) out[i] = pl.out[i];
+    return MT_OK;
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+const char* mt_status_str(mt_status s) {
+  switch (s) {
+    case MT_OK: return "ok";
+    case MT_ERR_NULL: return "null pointer";
+    case MT_ERR_NDIM: return "bad rank";
+    case MT_ERR_SHAPE: return "shape mismatch";
+    case MT_ERR_DTYPE: return "unsupported dtype";
+    case MT_ERR_LAYOUT: return "unsupported layout";
+    case MT_ERR_ALIAS: return "output overlaps input";
+    case MT_ERR_WORKSPACE: return "bad workspace";
+    case MT_ERR_HIP: return "HIP runtime error";
+    case MT_ERR_INVALID: return "invalid argument";
+  }
+  return "unknown status";
+}
+
+const char* mt_last_error(void) { return g_err.c_str(); }
+
+int mt_debug_set(const char* key, int64_t value) {
+  if (!key) return -1;
+  if (!std::strcmp(key, "cfg")) g_force_cfg = (int)value;
+  else if (!std::strcmp(key, "vec1")) g_force_vec1 = (int)value;
+  else if (!std::strcmp(key, "splits")) g_force_splits = (int)value;
+  else if (!std::strcmp(key, "parts")) g_force_parts = (int)value;
+  else return -1;
+  return 0;
+}
+
+}  // extern "C"

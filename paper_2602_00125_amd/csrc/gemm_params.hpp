@@ -1,0 +1,46 @@
+// Launch description shared by the host dispatch and the GEMM kernels.
+//
+// C[beta][m][n] (+)= sum_r sum_k A[beta, r][m][k] * B[beta, r][k][n] (+ bias[n])
+//
+// beta runs over the kept batch elements of the output, r over batch axes that
+// are summed into the output (the gradient of a broadcast operand); both are
+// decoded from flat indices with the per-dim sizes and element strides below.
+// An operand is "K-contiguous" when its k index has stride 1, otherwise its
+// m (for A) or n (for B) index has stride 1; `lda`/`ldb` is the stride of the
+// other matrix index. C is row-major with row pitch `ldc`.
+#pragma once
+#include <cstdint>
+
+namespace mt {
+
+constexpr int kMaxBatchDims = 6;
+
+struct GemmParams {
+  const void* a;
+  const void* b;
+  float* c;
+  const float* bias;  // nullable, length N, contiguous
+  int64_t M, N, K;
+  int64_t lda, ldb, ldc;
+  // kept batch dims (output batch elements), outermost first
+  int32_t nkeep;
+  int32_t nred;
+  int64_t keep_shape[kMaxBatchDims];
+  int64_t keep_sa[kMaxBatchDims], keep_sb[kMaxBatchDims], keep_sc[kMaxBatchDims];
+  // summed batch dims
+  int64_t red_shape[kMaxBatchDims];
+  int64_t red_sa[kMaxBatchDims], red_sb[kMaxBatchDims];
+  int64_t keep_count;  // product of keep_shape (1 if none)
+  int64_t red_count;   // product of red_shape (1 if none)
+  int32_t tiles_m, tiles_n;
+  int32_t accumulate;  // C += result
+  int32_t group_m;     // tile-order group height (L2 reuse)
+  // split-K: the k range is cut into `splits` slices; slice s of block writes
+  // its partial tile to `partial + s * partial_stride` (row-major, pitch N)
+  int32_t splits;
+  int64_t k_per_split;   // multiple of the kernel's BK
+  float* partial;
+  int64_t partial_stride;
+};
+
+}  // namespace mt
