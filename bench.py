@@ -29,14 +29,20 @@ BF16_MFMA_PEAK_TFLOPS = 2516.6  # MI355X dense bf16 matrix peak
 HBM_PEAK_GBS = 8000.0
 METRIC = "TFLOP/s for linear fwd+bwd (3 GEMMs) at M=N=K=8192 fp32; % MFMA peak"
 
-# sources whose text decides the measured kernels (for staleness of counters)
-KERNEL_SOURCES = ["paper_2602_00125_amd/csrc/gemm_f32.hip", "paper_2602_00125_amd/csrc/reduce.hip",
-                  "paper_2602_00125_amd/csrc/gemm_bf16.hip", "paper_2602_00125_amd/csrc/capi.cpp"]
+# sources whose text decides each measured kernel (counters taken on other
+# sources are stale and not reported)
+KERNEL_SOURCES = {
+    "gemm": ["paper_2602_00125_amd/csrc/gemm_f32.hip", "paper_2602_00125_amd/csrc/gemm_params.hpp",
+             "paper_2602_00125_amd/csrc/capi.cpp"],
+    "gemm_bf16": ["paper_2602_00125_amd/csrc/gemm_bf16.hip", "paper_2602_00125_amd/csrc/gemm_params.hpp",
+                  "paper_2602_00125_amd/csrc/capi.cpp"],
+    "colsum": ["paper_2602_00125_amd/csrc/reduce.hip", "paper_2602_00125_amd/csrc/capi.cpp"],
+}
 
 
-def sources_hash() -> str:
+def sources_hash(family: str) -> str:
     h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
+    for rel in KERNEL_SOURCES[family]:
         p = os.path.join(ROOT, rel)
         if os.path.exists(p):
             h.update(rel.encode())
@@ -52,7 +58,22 @@ def parse():
     ap.add_argument("--workload", default="linear_8192x8192x8192_f32")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target wall time of the CPU-oracle baseline sample (0 disables it)")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB (calibrates HBM "
+                         "byte counters against a kernel of known traffic) and exit")
     return ap.parse_args()
+
+
+def copy_probe(mib: int) -> None:
+    import torch
+
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4}))
 
 
 def cpu_baseline(inp, seconds: float):
@@ -98,6 +119,9 @@ def cpu_baseline(inp, seconds: float):
 
 def main():
     args = parse()
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "
               f"multi-GPU path", file=sys.stderr)
@@ -169,7 +193,8 @@ def main():
     if os.path.exists(tfile):
         try:
             rec = json.load(open(tfile)).get(args.workload, {}).get(dominant)
-            if rec and rec.get("sources_hash") == sources_hash():
+            fam = "gemm_bf16" if is_bf16 else "gemm"
+            if rec and rec.get("sources_hash") == sources_hash(fam):
                 traffic = rec["hbm_bytes_per_launch"]
         except (ValueError, OSError):
             traffic = None
