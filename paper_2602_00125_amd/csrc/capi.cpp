@@ -117,39 +117,44 @@ void init_params(mt::GemmParams* p) {
 struct GemmCall {
   mt::GemmParams p;
   bool a_kc, b_kc;
-  bool vec4;
+  bool vec;   // 16-byte operand loads and output stores
+  bool bf16;  // bf16 operands (else fp32)
   int cfg;
 };
 
-// Everything the fp32 kernels need checked for 16-byte vector access.
-bool vec4_ok_operand(const void* base, bool kc, int64_t rows_other, int64_t contig_extent,
-                     int64_t ld, const int64_t* bstrides, int nb) {
-  if (!aligned16(base) || contig_extent % 4 != 0) return false;
-  if (rows_other > 1 && ld % 4 != 0) return false;
+// Whether an operand allows 16-byte loads: `per` elements per vector (4 fp32,
+// 8 bf16) must divide its contiguous extent, its pitch and every batch
+// stride, and its base must be 16-byte aligned.
+bool vec_ok_operand(const void* base, int64_t rows_other, int64_t contig_extent, int64_t ld,
+                    const int64_t* bstrides, int nb, int per) {
+  if (!aligned16(base) || contig_extent % per != 0) return false;
+  if (rows_other > 1 && ld % per != 0) return false;
   for (int i = 0; i < nb; ++i)
-    if (bstrides[i] % 4 != 0) return false;
-  (void)kc;
+    if (bstrides[i] % per != 0) return false;
   return true;
 }
+
+int vec_elems(bool bf16) { return bf16 ? 8 : 4; }
 
 mt_status launch_gemm(GemmCall& g, hipStream_t stream, void* ws, size_t ws_bytes) {
   mt::GemmParams& p = g.p;
   if (p.M == 0 || p.N == 0 || p.keep_count == 0) return MT_OK;
   if (g.cfg < 0) g.cfg = choose_cfg(p.M, p.N, p.keep_count);
-  if (g_force_vec1) g.vec4 = false;
-  // the 4-byte-load kernels keep their staging registers within budget up to 128x128
-  if (!g.vec4 && (g.cfg == mt::kCfg256x256 || g.cfg == mt::kCfg256x128 || g.cfg == mt::kCfg128x256))
+  if (g_force_vec1) g.vec = false;
+  // the element-load kernels keep their staging registers within budget up to 128x128
+  if (!g.vec && (g.cfg == mt::kCfg256x256 || g.cfg == mt::kCfg256x128 || g.cfg == mt::kCfg128x256))
     g.cfg = mt::kCfg128x128;
   // 32-bit buffer offsets: one tile's rows times the row pitch must stay below 2 GiB
-  const int64_t rows_a = g.a_kc ? mt::gemm_tile_m(g.cfg) : mt::gemm_tile_k(g.cfg);
-  const int64_t rows_b = g.b_kc ? mt::gemm_tile_n(g.cfg) : mt::gemm_tile_k(g.cfg);
-  if (rows_a * p.lda * 4 >= (int64_t)1 << 31 || rows_b * p.ldb * 4 >= (int64_t)1 << 31)
+  const int64_t es = g.bf16 ? 2 : 4;
+  const int64_t rows_a = g.a_kc ? mt::gemm_tile_m(g.cfg) : mt::gemm_tile_k(g.cfg, g.bf16);
+  const int64_t rows_b = g.b_kc ? mt::gemm_tile_n(g.cfg) : mt::gemm_tile_k(g.cfg, g.bf16);
+  if (rows_a * p.lda * es >= (int64_t)1 << 31 || rows_b * p.ldb * es >= (int64_t)1 << 31)
     return fail(MT_ERR_LAYOUT, "row pitch too large for 32-bit tile offsets");
   p.splits = 1;
   p.k_per_split = p.K > 0 ? p.K : 1;
   if (ws && p.keep_count == 1 && p.red_count == 1) {
     const int s = choose_splits(p.M, p.N, p.K, g.cfg);
-    const int64_t bk = mt::gemm_tile_k(g.cfg);
+    const int64_t bk = mt::gemm_tile_k(g.cfg, g.bf16);
     if (s > 1) {
       const int64_t kps = ((p.K + s - 1) / s + bk - 1) / bk * bk;
       const int splits = (int)((p.K + kps - 1) / kps);
@@ -163,7 +168,8 @@ mt_status launch_gemm(GemmCall& g, hipStream_t stream, void* ws, size_t ws_bytes
     }
   }
   (void)hipGetLastError();  // clear a stale error so the launch check is ours
-  hipError_t e = mt::gemm_f32(p, g.a_kc, g.b_kc, g.vec4, g.cfg, stream);
+  hipError_t e = g.bf16 ? mt::gemm_bf16(p, g.a_kc, g.b_kc, g.vec, g.cfg, stream)
+                        : mt::gemm_f32(p, g.a_kc, g.b_kc, g.vec, g.cfg, stream);
   if (e != hipSuccess) return hip_status(e);
   if (p.splits > 1) {
     e = mt::splitk_finish(p.partial, p.splits, p.M, p.N, p.c, p.ldc, p.bias, p.accumulate != 0,
@@ -237,7 +243,8 @@ mt_status linear_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tenso
     if (dw->shape[0] != N || dw->shape[1] != K) return fail(MT_ERR_SHAPE, "dw must be [N, K]");
   }
   if (db && (s = check_vector(db, "db", N))) return s;
-  if (dt == MT_BF16) return fail(MT_ERR_DTYPE, "bf16 operands are not supported yet");
+  const bool bf = dt == MT_BF16;
+  const int per = vec_elems(bf);
   // inputs actually read: dy always, x for dw, w for dx
   const mt_tensor* ins[3] = {dy, dw ? x : nullptr, dx ? w : nullptr};
   const mt_tensor* outs[3] = {dx, dw, db};
@@ -267,9 +274,10 @@ mt_status linear_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tenso
     gdw.p.accumulate = acc;
     gdw.a_kc = false;
     gdw.b_kc = false;
-    gdw.vec4 = vec4_ok_operand(dy->data, false, M, N, gdw.p.lda, nullptr, 0) &&
-               vec4_ok_operand(x->data, false, M, K, gdw.p.ldb, nullptr, 0) &&
-               aligned16(dw->data) && K % 4 == 0 && gdw.p.ldc % 4 == 0;
+    gdw.bf16 = bf;
+    gdw.vec = vec_ok_operand(dy->data, M, N, gdw.p.lda, nullptr, 0, per) &&
+              vec_ok_operand(x->data, M, K, gdw.p.ldb, nullptr, 0, per) &&
+              aligned16(dw->data) && K % 4 == 0 && gdw.p.ldc % 4 == 0;
     gdw.cfg = choose_cfg(N, K, 1);
     const int sp = choose_splits(N, K, M, gdw.cfg);
     if (sp > 1) need_dw = (size_t)sp * N * K * sizeof(float);
@@ -301,9 +309,10 @@ mt_status linear_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tenso
     g.p.accumulate = acc;
     g.a_kc = true;
     g.b_kc = false;
-    g.vec4 = vec4_ok_operand(dy->data, true, M, N, g.p.lda, nullptr, 0) &&
-             vec4_ok_operand(w->data, false, N, K, g.p.ldb, nullptr, 0) && aligned16(dx->data) &&
-             K % 4 == 0 && g.p.ldc % 4 == 0;
+    g.bf16 = bf;
+    g.vec = vec_ok_operand(dy->data, M, N, g.p.lda, nullptr, 0, per) &&
+            vec_ok_operand(w->data, N, K, g.p.ldb, nullptr, 0, per) && aligned16(dx->data) &&
+            K % 4 == 0 && g.p.ldc % 4 == 0;
     g.cfg = -1;
     if ((s = launch_gemm(g, stream, nullptr, 0))) return s;
   }
@@ -313,7 +322,7 @@ mt_status linear_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tenso
   if (db && N > 0) {
     (void)hipGetLastError();
     float* wsp = (ws && parts > 1 && ws_bytes >= need_db) ? (float*)ws : nullptr;
-    hipError_t e = mt::colsum(dy->data, dt == MT_BF16, M, N, pitch(dy), (float*)db->data, acc,
+    hipError_t e = mt::colsum(dy->data, bf, M, N, pitch(dy), (float*)db->data, acc,
                               wsp, parts, stream);
     if (e != hipSuccess) return hip_status(e);
   }
@@ -329,7 +338,6 @@ mt_status matmul_impl(const mt_tensor* a, const mt_tensor* b, const mt_tensor* c
   if ((s = check_tensor(c, "c", 0, MT_MAX_DIMS))) return s;
   if (a->dtype != b->dtype) return fail(MT_ERR_DTYPE, "a and b must share a dtype");
   if (c->dtype != MT_F32) return fail(MT_ERR_DTYPE, "c must be f32");
-  if (a->dtype == MT_BF16) return fail(MT_ERR_DTYPE, "bf16 operands are not supported yet");
   mt::MatmulPlan pl;
   std::string err;
   if ((s = mt::plan_matmul_shapes(a->ndim, a->shape, a->stride, b->ndim, b->shape, b->stride, &pl,
@@ -399,13 +407,15 @@ mt_status matmul_impl(const mt_tensor* a, const mt_tensor* b, const mt_tensor* c
   if (p.red_count == 0) g.p.K = 0;  // an empty summed batch contributes nothing
   g.a_kc = a_kc;
   g.b_kc = b_kc;
+  g.bf16 = a->dtype == MT_BF16;
+  const int per = vec_elems(g.bf16);
   int64_t sa_all[2 * MT_MAX_DIMS], sb_all[2 * MT_MAX_DIMS];
   int na = 0;
   for (int i = 0; i < p.nkeep; ++i) { sa_all[na] = p.keep_sa[i]; sb_all[na++] = p.keep_sb[i]; }
   for (int i = 0; i < p.nred; ++i) { sa_all[na] = p.red_sa[i]; sb_all[na++] = p.red_sb[i]; }
-  g.vec4 = vec4_ok_operand(a->data, a_kc, a_kc ? pl.M : pl.K, a_kc ? pl.K : pl.M, lda, sa_all, na) &&
-           vec4_ok_operand(b->data, b_kc, b_kc ? pl.N : pl.K, b_kc ? pl.K : pl.N, ldb, sb_all, na) &&
-           aligned16(c->data) && pl.N % 4 == 0;
+  g.vec = vec_ok_operand(a->data, a_kc ? pl.M : pl.K, a_kc ? pl.K : pl.M, lda, sa_all, na, per) &&
+          vec_ok_operand(b->data, b_kc ? pl.N : pl.K, b_kc ? pl.K : pl.N, ldb, sb_all, na, per) &&
+          aligned16(c->data) && pl.N % 4 == 0;
   g.cfg = -1;
   return launch_gemm(g, stream, nullptr, 0);
 }
@@ -453,7 +463,8 @@ mt_status mt_linear_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
     if (w->shape[1] != K) return fail(MT_ERR_SHAPE, "w must be [N, K] with x [M, K]");
     if (y->shape[0] != M || y->shape[1] != N) return fail(MT_ERR_SHAPE, "y must be [M, N]");
     if (b && (s = check_vector(b, "b", N))) return s;
-    if (x->dtype == MT_BF16) return fail(MT_ERR_DTYPE, "bf16 operands are not supported yet");
+    const bool bf = x->dtype == MT_BF16;
+    const int per = vec_elems(bf);
     if (overlaps(y, x) || overlaps(y, w) || overlaps(y, b))
       return fail(MT_ERR_ALIAS, "y overlaps an input");
     if (M == 0 || N == 0) return MT_OK;
@@ -471,9 +482,10 @@ mt_status mt_linear_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
     g.p.ldc = pitch(y);
     g.a_kc = true;
     g.b_kc = true;
-    g.vec4 = vec4_ok_operand(x->data, true, M, K, g.p.lda, nullptr, 0) &&
-             vec4_ok_operand(w->data, true, N, K, g.p.ldb, nullptr, 0) && aligned16(y->data) &&
-             N % 4 == 0 && g.p.ldc % 4 == 0 && (!g.p.bias || aligned16(g.p.bias));
+    g.bf16 = bf;
+    g.vec = vec_ok_operand(x->data, M, K, g.p.lda, nullptr, 0, per) &&
+            vec_ok_operand(w->data, N, K, g.p.ldb, nullptr, 0, per) && aligned16(y->data) &&
+            N % 4 == 0 && g.p.ldc % 4 == 0 && (!g.p.bias || aligned16(g.p.bias));
     g.cfg = -1;
     return launch_gemm(g, (hipStream_t)stream, nullptr, 0);
   } catch (...) {

@@ -12,12 +12,16 @@ namespace mt {
 enum GemmCfg { kCfg256x256 = 0, kCfg256x128 = 1, kCfg128x256 = 2, kCfg128x128 = 3, kCfg64x64 = 4 };
 int gemm_tile_m(int cfg);
 int gemm_tile_n(int cfg);
-int gemm_tile_k(int cfg);
+int gemm_tile_k(int cfg, bool bf16);
 
-// fp32 operands. vec4: 16-byte loads/stores (the host has checked that every
-// contiguous extent, pitch, batch stride and base allows them).
-hipError_t gemm_f32(const GemmParams& p, bool a_kc, bool b_kc, bool vec4, int cfg,
+// fp32 operands. vec: 16-byte loads/stores (the host has checked that every
+// contiguous extent, pitch, batch stride and base allows them); else 4-byte.
+hipError_t gemm_f32(const GemmParams& p, bool a_kc, bool b_kc, bool vec, int cfg,
                     hipStream_t stream);
+// bf16 operands (fp32 accumulation, bias and output). vec: 16-byte loads
+// (8 elements) and 16-byte stores; else 2-byte loads and 4-byte stores.
+hipError_t gemm_bf16(const GemmParams& p, bool a_kc, bool b_kc, bool vec, int cfg,
+                     hipStream_t stream);
 
 // Split-K finish: C[m][n] (+)= sum_s partial[s][m][n] (+ bias[n]), s ascending.
 hipError_t splitk_finish(const float* partial, int splits, int64_t M, int64_t N, float* c,

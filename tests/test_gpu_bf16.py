@@ -1,0 +1,143 @@
+"""GPU parity of the bf16-operand dense layer and matmul (exact bf16
+products, fp32 accumulation, fp32 bias/outputs) against the fp64 oracle run
+on the identical bf16 values.
+
+Bar (reading R2 of the relative 2e-2 tolerance): elementwise
+|gpu - oracle| <= 2e-2 * S + 1e-6 and normwise ||gpu - oracle|| / ||oracle||
+<= 2e-2. Since bf16 x bf16 products are exact in fp32, the kernels should
+also meet the fp32 bar (1e-4 * S + 1e-6); that is checked as well.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2602_00125_amd import workloads as wl
+
+from helpers import assert_close, sample_positions, to_f64
+
+pytestmark = pytest.mark.gpu
+
+b = pytest.importorskip("paper_2602_00125_amd.binding")
+DEV = "cuda:0"
+
+
+def check_bf16(got, want, S, what):
+    assert_close(got, want, S, rel=2e-2, abs_=1e-6, what=what + " (bf16 bar)")
+    nrm = np.linalg.norm(want)
+    if nrm > 0:
+        assert np.linalg.norm(got - want) / nrm <= 2e-2, what
+    assert_close(got, want, S, what=what + " (fp32 bar)")
+
+
+def make(M, N, K, seed, dist=None):
+    return wl.linear(M, N, K, dtype="bf16", seed=seed, dist=dist).make()
+
+
+def run(inp):
+    x, w, bias, dy = (inp[k].to(DEV) for k in ("X", "W", "b", "dY"))
+    M, K = x.shape
+    N = w.shape[0]
+    y = torch.full((M, N), float("nan"), device=DEV)
+    dx = torch.full((M, K), float("nan"), device=DEV)
+    dw = torch.full((N, K), float("nan"), device=DEV)
+    db = torch.full((N,), float("nan"), device=DEV)
+    b.linear_fwd(x, w, bias, y)
+    n = b.linear_bwd_workspace(x, w, dy, dx, dw, db)
+    ws = torch.empty(n // 4 + 64, device=DEV) if n else None
+    b.linear_bwd(x, w, dy, dx, dw, db, workspace=ws)
+    torch.cuda.synchronize()
+    return {"Y": y, "dX": dx, "dW": dw, "db": db}
+
+
+def check_full(inp, out):
+    X, W, B, dY = (to_f64(inp[k]) for k in ("X", "W", "b", "dY"))
+    Y, SY = oracle.linear_fwd(X, W, B)
+    check_bf16(to_f64(out["Y"]), Y, SY, "Y")
+    dX, SX = oracle.linear_bwd_dx(dY, W)
+    check_bf16(to_f64(out["dX"]), dX, SX, "dX")
+    dW, SW = oracle.linear_bwd_dw(dY, X)
+    check_bf16(to_f64(out["dW"]), dW, SW, "dW")
+    db, Sb = oracle.linear_bwd_db(dY)
+    check_bf16(to_f64(out["db"]), db, Sb, "db")
+
+
+@pytest.mark.parametrize("M,N,K", [(64, 32, 128), (300, 200, 100), (520, 392, 264), (257, 129, 67),
+                                   (1, 1, 1), (96, 1000, 40), (1000, 96, 40)])
+def test_bf16_linear_small_and_ragged(M, N, K):
+    inp = make(M, N, K, seed=M + N + K)
+    check_full(inp, run(inp))
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("vec1", [0, 1])
+def test_bf16_every_tile_config(cfg, vec1):
+    inp = make(520, 392, 264, seed=17)
+    b.debug_set("cfg", cfg)
+    b.debug_set("vec1", vec1)
+    try:
+        out = run(inp)
+    finally:
+        b.debug_set("cfg", -1)
+        b.debug_set("vec1", 0)
+    check_full(inp, out)
+
+
+def test_bf16_linear_16384x8192x8192_sampled():
+    inp = wl.LINEAR_16384x8192x8192_BF16.make()
+    out = run(inp)
+    X, W, B, dY = (to_f64(inp[k]) for k in ("X", "W", "b", "dY"))
+    M, K = X.shape
+    N = W.shape[0]
+    r, c = sample_positions(M, N, 3000, seed=1)
+    v, S = oracle.linear_fwd_at(X, W, B, r, c)
+    check_bf16(to_f64(out["Y"])[r, c], v, S, "Y (sampled)")
+    r, c = sample_positions(M, K, 3000, seed=2)
+    v, S = oracle.linear_bwd_dx_at(dY, W, r, c)
+    check_bf16(to_f64(out["dX"])[r, c], v, S, "dX (sampled)")
+    r, c = sample_positions(N, K, 3000, seed=3)
+    v, S = oracle.linear_bwd_dw_at(dY, X, r, c)
+    check_bf16(to_f64(out["dW"])[r, c], v, S, "dW (sampled)")
+    db, Sb = oracle.linear_bwd_db(dY)
+    check_bf16(to_f64(out["db"]), db, Sb, "db")
+    for k in out:
+        assert torch.isfinite(out[k]).all(), k
+
+
+def test_bf16_integer_inputs_bit_exact_at_16384x8192x8192():
+    """Integers in [-4, 4] are exact in bf16 and every partial sum stays below
+    2**24, so the result is exact in any summation order."""
+    inp = make(16384, 8192, 8192, seed=6, dist={k: wl.integers(-4, 4) for k in ("X", "W", "b", "dY")})
+    out = run(inp)
+    X, W, B, dY = (to_f64(inp[k]) for k in ("X", "W", "b", "dY"))
+    for k in out:
+        assert torch.equal(out[k], torch.round(out[k])), k
+    r, c = sample_positions(16384, 8192, 2000, seed=7)
+    assert np.array_equal(to_f64(out["Y"])[r, c], oracle.linear_fwd_at(X, W, B, r, c)[0])
+    assert np.array_equal(to_f64(out["dX"])[r, c], oracle.linear_bwd_dx_at(dY, W, r, c)[0])
+    r, c = sample_positions(8192, 8192, 2000, seed=8)
+    assert np.array_equal(to_f64(out["dW"])[r, c], oracle.linear_bwd_dw_at(dY, X, r, c)[0])
+    assert np.array_equal(to_f64(out["db"]), oracle.linear_bwd_db(dY)[0])
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_bf16_broadcast_matmul(seed):
+    rng = np.random.default_rng(100 + seed)
+    M, K, N = (int(rng.choice([5, 32, 77, 128, 200])) for _ in range(3))
+    A = wl.tensor((3, 1, M, K), ("normal",), seed=seed).to(torch.bfloat16)
+    B = wl.tensor((1, 2, K, N), ("normal",), seed=seed + 50).to(torch.bfloat16)
+    dC = wl.tensor((3, 2, M, N), ("normal",), seed=seed + 99).to(torch.bfloat16)
+    Ad, Bd, dCd = A.to(DEV), B.to(DEV), dC.to(DEV)
+    C = torch.empty(3, 2, M, N, device=DEV)
+    b.matmul(Ad, Bd, C)
+    dA = torch.empty(3, 1, M, K, device=DEV)
+    dB = torch.empty(1, 2, K, N, device=DEV)
+    b.matmul(dCd, Bd.transpose(-1, -2), dA, reduce_into=True)
+    b.matmul(Ad.transpose(-1, -2), dCd, dB, reduce_into=True)
+    torch.cuda.synchronize()
+    An, Bn, dCn = to_f64(A), to_f64(B), to_f64(dC)
+    Cr, SC = oracle.matmul(An, Bn)
+    check_bf16(to_f64(C), Cr, SC, "C")
+    dAr, SA, dBr, SB = oracle.matmul_bwd(An, Bn, dCn)
+    check_bf16(to_f64(dA), dAr, SA, "dA")
+    check_bf16(to_f64(dB), dBr, SB, "dB")
