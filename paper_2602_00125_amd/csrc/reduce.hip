@@ -4,10 +4,12 @@
 //   bias (MiniTensor Sec. 3.2 add pullback with the Sec. 3.1 broadcasting
 //   rule; Sec. 3.3 Eq. (5)). The summed axis is the outer (strided) one, so
 //   lanes run along the contiguous n (16-byte loads, 4 columns a lane) and
-//   the four waves of a block take interleaved rows; their partial sums are
-//   combined through LDS in a fixed order. Large M is cut into row slices
-//   whose sums go to a workspace and are added by a second pass in slice
-//   order: no atomics, bit-identical reruns.
+//   the sixteen waves of a block take interleaved rows with four loads in
+//   flight per lane (64 KB per CU in flight keeps HBM busy); their partial
+//   sums are combined through LDS in a fixed order. M is cut into row slices
+//   so that about one block runs per CU; slice sums go to a workspace and
+//   are added by a second pass in slice order: no atomics, bit-identical
+//   reruns.
 // * reduce_strided: the same add pullback for any broadcast (the gradient of
 //   an operand that was expanded along some axes). When the innermost axis
 //   of the gradient is kept, a thread per output walks the summed axes
@@ -45,13 +47,14 @@ __device__ __forceinline__ float load1(const void* base, int64_t idx) {
   else return ((const float*)base)[idx];
 }
 
-// grid: (ceil(N / (64*VEC)), parts). Block 256 = 4 waves; wave w sums rows
-// r0 + w, r0 + w + 4, ... of its slice for 64*VEC columns.
-template <bool BF16, int VEC>
-__global__ __launch_bounds__(256) void colsum_kernel(const void* x, int64_t M, int64_t N, int64_t ld,
-                                                     float* out, int accumulate, float* ws,
-                                                     int64_t rows_per_part) {
-  __shared__ f32x4 red[4][64];
+// grid: (ceil(N / (64*VEC)), parts). Block = WAVES wave64s; wave w sums rows
+// r0 + w, r0 + w + WAVES, ... of its slice for 64*VEC columns, four rows in
+// flight per lane; the WAVES partial sums meet in LDS in wave order.
+template <bool BF16, int VEC, int WAVES>
+__global__ __launch_bounds__(WAVES * 64) void colsum_kernel(const void* x, int64_t M, int64_t N,
+                                                            int64_t ld, float* out, int accumulate,
+                                                            float* ws, int64_t rows_per_part) {
+  __shared__ f32x4 red[WAVES][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t n = ((int64_t)blockIdx.x * 64 + lane) * VEC;
   const int64_t r0 = (int64_t)blockIdx.y * rows_per_part;
@@ -60,29 +63,27 @@ __global__ __launch_bounds__(256) void colsum_kernel(const void* x, int64_t M, i
   if (n < N) {
     if (VEC == 4) {
       int64_t m = r0 + wave;
-      // four independent rows in flight per iteration
-      for (; m + 12 < r1; m += 16) {
+      for (; m + 3 * WAVES < r1; m += 4 * WAVES) {
         const f32x4 a = load4<BF16>(x, m * ld + n);
-        const f32x4 b = load4<BF16>(x, (m + 4) * ld + n);
-        const f32x4 c = load4<BF16>(x, (m + 8) * ld + n);
-        const f32x4 d = load4<BF16>(x, (m + 12) * ld + n);
+        const f32x4 b = load4<BF16>(x, (m + WAVES) * ld + n);
+        const f32x4 c = load4<BF16>(x, (m + 2 * WAVES) * ld + n);
+        const f32x4 d = load4<BF16>(x, (m + 3 * WAVES) * ld + n);
         acc += a;
         acc += b;
         acc += c;
         acc += d;
       }
-      for (; m < r1; m += 4) acc += load4<BF16>(x, m * ld + n);
+      for (; m < r1; m += WAVES) acc += load4<BF16>(x, m * ld + n);
     } else {
-      for (int64_t m = r0 + wave; m < r1; m += 4) acc[0] += load1<BF16>(x, m * ld + n);
+      for (int64_t m = r0 + wave; m < r1; m += WAVES) acc[0] += load1<BF16>(x, m * ld + n);
     }
   }
   red[wave][lane] = acc;
   __syncthreads();
   if (wave == 0 && n < N) {
     f32x4 s = red[0][lane];
-    s += red[1][lane];
-    s += red[2][lane];
-    s += red[3][lane];
+#pragma unroll
+    for (int w = 1; w < WAVES; ++w) s += red[w][lane];
     if (gridDim.y > 1) {
       float* dst = ws + (int64_t)blockIdx.y * N;
       for (int e = 0; e < VEC; ++e)
@@ -94,13 +95,22 @@ __global__ __launch_bounds__(256) void colsum_kernel(const void* x, int64_t M, i
   }
 }
 
-// out[n] (+)= sum_p ws[p][n], p ascending.
+// out[n] (+)= sum_p ws[p][n], p ascending (loads issued four at a time).
 __global__ __launch_bounds__(256) void parts_finish_kernel(const float* ws, int parts, int64_t N,
                                                            float* out, int accumulate) {
   const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (n >= N) return;
   float s = 0.f;
-  for (int p = 0; p < parts; ++p) s += ws[(int64_t)p * N + n];
+  int p = 0;
+  for (; p + 3 < parts; p += 4) {
+    const float a = ws[(int64_t)p * N + n], b = ws[(int64_t)(p + 1) * N + n];
+    const float c = ws[(int64_t)(p + 2) * N + n], d = ws[(int64_t)(p + 3) * N + n];
+    s += a;
+    s += b;
+    s += c;
+    s += d;
+  }
+  for (; p < parts; ++p) s += ws[(int64_t)p * N + n];
   out[n] = accumulate ? out[n] + s : s;
 }
 
@@ -183,14 +193,17 @@ __global__ __launch_bounds__(256) void reduce_inner_kernel(const float* x, const
 
 }  // namespace
 
+constexpr int kColsumWaves = 16;
+
 int colsum_parts(int64_t M, int64_t N) {
-  // aim for ~2048 blocks of at least 64 rows each
+  // one block per CU: (columns / 256) x parts ~ 256 blocks, slices of at
+  // least 256 rows
   const int64_t col_blocks = (N + 255) / 256;
-  int64_t parts = 2048 / (col_blocks > 0 ? col_blocks : 1);
-  const int64_t max_parts = M / 64;
+  int64_t parts = 256 / (col_blocks > 0 ? col_blocks : 1);
+  const int64_t max_parts = M / 256;
   if (parts > max_parts) parts = max_parts;
   if (parts < 1) parts = 1;
-  if (parts > 1024) parts = 1024;
+  if (parts > 256) parts = 256;
   return (int)parts;
 }
 
@@ -203,20 +216,21 @@ hipError_t colsum(const void* x, bool is_bf16, int64_t M, int64_t N, int64_t ld,
   const int V = vec ? 4 : 1;
   const int64_t rows_per_part = M > 0 ? (M + parts - 1) / parts : 0;
   dim3 grid((unsigned)((N + 64 * V - 1) / (64 * V)), (unsigned)parts);
+  dim3 block(kColsumWaves * 64);
   if (vec) {
     if (is_bf16)
-      hipLaunchKernelGGL((colsum_kernel<true, 4>), grid, dim3(256), 0, stream, x, M, N, ld, out,
-                         (int)accumulate, ws, rows_per_part);
+      hipLaunchKernelGGL((colsum_kernel<true, 4, kColsumWaves>), grid, block, 0, stream, x, M, N, ld,
+                         out, (int)accumulate, ws, rows_per_part);
     else
-      hipLaunchKernelGGL((colsum_kernel<false, 4>), grid, dim3(256), 0, stream, x, M, N, ld, out,
-                         (int)accumulate, ws, rows_per_part);
+      hipLaunchKernelGGL((colsum_kernel<false, 4, kColsumWaves>), grid, block, 0, stream, x, M, N, ld,
+                         out, (int)accumulate, ws, rows_per_part);
   } else {
     if (is_bf16)
-      hipLaunchKernelGGL((colsum_kernel<true, 1>), grid, dim3(256), 0, stream, x, M, N, ld, out,
-                         (int)accumulate, ws, rows_per_part);
+      hipLaunchKernelGGL((colsum_kernel<true, 1, kColsumWaves>), grid, block, 0, stream, x, M, N, ld,
+                         out, (int)accumulate, ws, rows_per_part);
     else
-      hipLaunchKernelGGL((colsum_kernel<false, 1>), grid, dim3(256), 0, stream, x, M, N, ld, out,
-                         (int)accumulate, ws, rows_per_part);
+      hipLaunchKernelGGL((colsum_kernel<false, 1, kColsumWaves>), grid, block, 0, stream, x, M, N, ld,
+                         out, (int)accumulate, ws, rows_per_part);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || parts == 1) return e;
