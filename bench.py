@@ -117,6 +117,77 @@ def cpu_baseline(inp, seconds: float):
                       f"products with the |a*b| bound) in {el:.1f} s; TFLOP/s = 2*MACs/s"}
 
 
+def timed_steps(step, n_events: int, steps: int, warmup: int):
+    """Warm up, then time `steps` steps with events between their calls."""
+    import torch
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(n_events)] for _ in range(steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for i in range(steps):
+        step(events[i])
+    t1.record()
+    torch.cuda.synchronize()
+    per = [0.0] * (n_events - 1)
+    for ev in events:
+        for j in range(n_events - 1):
+            per[j] += ev[j].elapsed_time(ev[j + 1])
+    return t0.elapsed_time(t1) / steps, [v / steps for v in per]
+
+
+def bench_bmm(args, w, inp, dev):
+    """Broadcasting batched matmul step: C = A @ B, then dA and dB with the
+    broadcast-axis sums folded into the products (MT_REDUCE_INTO)."""
+    import torch
+
+    from paper_2602_00125_amd import binding as mt
+
+    A, B, dC = (inp[k].to(dev) for k in ("A", "B", "dC"))
+    C = torch.empty(w.cshape, device=dev)
+    dA = torch.empty(w.ashape, device=dev)
+    dB = torch.empty(w.bshape, device=dev)
+    Bt, At = B.transpose(-1, -2), A.transpose(-1, -2)
+    need = max(mt.matmul_workspace(A, B, C), mt.matmul_workspace(dC, Bt, dA, reduce_into=True),
+               mt.matmul_workspace(At, dC, dB, reduce_into=True))
+    ws = torch.empty(need // 4 + 64, device=dev) if need else None
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        mt.matmul(A, B, C, workspace=ws)
+        if ev is not None:
+            ev[1].record()
+        mt.matmul(dC, Bt, dA, reduce_into=True, workspace=ws)
+        if ev is not None:
+            ev[2].record()
+        mt.matmul(At, dC, dB, reduce_into=True, workspace=ws)
+        if ev is not None:
+            ev[3].record()
+
+    ms, per = timed_steps(step, 4, args.steps, args.warmup)
+    names = ["fwd_gemm", "dA_gemm_reduce_into", "dB_gemm_reduce_into"]
+    per = dict(zip(names, per))
+    value = w.flops() / (ms * 1e-3) / 1e12
+    dominant = max(names, key=lambda k: per[k])
+    achieved = (w.flops() / 3) / (per[dominant] * 1e-3) / 1e12
+    out = {"metric": f"TFLOP/s for broadcast matmul fwd+bwd (3 products) on {args.workload}",
+           "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": args.workload, "a": list(w.ashape), "b": list(w.bshape),
+                      "pct_of_mfma_peak": round(100.0 * value / FP32_MFMA_PEAK_TFLOPS, 2)},
+           "roofline": {"bound": "mfma", "kernel": dominant, "achieved": round(achieved, 3),
+                        "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                        "frac": round(achieved / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": None},
+           "kernels_ms": {k: round(v, 4) for k, v in per.items()}, "cpu_baseline": None}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_probe:
@@ -132,9 +203,10 @@ def main():
     from paper_2602_00125_amd import workloads as wl
 
     w = wl.WORKLOADS[args.workload]
-    assert isinstance(w, wl.LinearWorkload), "the bench times the dense-layer step"
     dev = torch.device("cuda:0")
     inp = w.make()
+    if isinstance(w, wl.BmmWorkload):
+        return bench_bmm(args, w, inp, dev)
     x, wt, bias, dy = (inp[k].to(dev) for k in ("X", "W", "b", "dY"))
     M, N, K = w.M, w.N, w.K
     y = torch.empty(M, N, device=dev)
@@ -160,24 +232,9 @@ def main():
         if ev is not None:
             ev[4].record()
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start.record()
-    for i in range(args.steps):
-        step(events[i])
-    t_end.record()
-    torch.cuda.synchronize()
-    total_ms = t_start.elapsed_time(t_end)
-    per = {"fwd_nt_gemm": 0.0, "dx_nn_gemm": 0.0, "dw_tn_gemm": 0.0, "db_colsum": 0.0}
-    for ev in events:
-        for j, k in enumerate(per):
-            per[k] += ev[j].elapsed_time(ev[j + 1])
-    per = {k: v / args.steps for k, v in per.items()}
+    total_ms_step, per_list = timed_steps(step, 5, args.steps, args.warmup)
+    per = dict(zip(["fwd_nt_gemm", "dx_nn_gemm", "dw_tn_gemm", "db_colsum"], per_list))
+    total_ms = total_ms_step * args.steps
     ms_per_step = total_ms / args.steps
     flops = w.flops()
     value = flops / (ms_per_step * 1e-3) / 1e12

@@ -100,7 +100,8 @@ mt_status mt_linear_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
  *   NULL when dw is NULL and w may be NULL when dx is NULL.
  * flags: MT_ACCUMULATE adds into dx/dw/db instead of overwriting.
  * ws/ws_bytes: optional workspace (size from mt_linear_bwd_workspace); used
- * for split reductions of db and split-K partial sums of dw.
+ * for split reductions of db and split-K partial sums of dx / dw when their
+ * output tiles under-fill the GPU.
  */
 mt_status mt_linear_bwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* dy,
                         const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db,
@@ -124,10 +125,17 @@ mt_status mt_linear_bwd_workspace(const mt_tensor* x, const mt_tensor* w, const 
  *     with exactly the result shape, or, with MT_REDUCE_INTO, that shape
  *     summed over some batch axes (leading axes dropped, kept axes of size
  *     1), i.e. the gradient of a broadcast operand.
- * flags: MT_ACCUMULATE, MT_REDUCE_INTO. ws is reserved (pass NULL/0).
+ * flags: MT_ACCUMULATE, MT_REDUCE_INTO.
+ * ws/ws_bytes: optional workspace (size from mt_matmul_workspace) for split-K
+ * partial sums when the output tiles alone under-fill the GPU (e.g. a
+ * gradient summed over broadcast axes, whose sum runs inside the product).
  */
 mt_status mt_matmul(const mt_tensor* a, const mt_tensor* b, const mt_tensor* c, uint32_t flags,
                     void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes mt_matmul can use for these arguments (0 if none). */
+mt_status mt_matmul_workspace(const mt_tensor* a, const mt_tensor* b, const mt_tensor* c,
+                              uint32_t flags, size_t* bytes);
 
 /* mt_reduce_broadcast_grad: the add pullback through a broadcast (Sec. 3.1,
  * Sec. 3.2): grad_in = grad_out summed over every axis along which an input

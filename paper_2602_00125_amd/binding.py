@@ -27,6 +27,7 @@ STATUS = {0: "MT_OK", 1: "MT_ERR_NULL", 2: "MT_ERR_NDIM", 3: "MT_ERR_SHAPE", 4: 
           9: "MT_ERR_INVALID"}
 
 EXPORTS = ["mt_linear_fwd", "mt_linear_bwd", "mt_linear_bwd_workspace", "mt_matmul",
+           "mt_matmul_workspace",
            "mt_reduce_broadcast_grad", "mt_reduce_broadcast_grad_workspace", "mt_broadcast_shape",
            "mt_matmul_shape", "mt_debug_set", "mt_status_str", "mt_last_error"]
 
@@ -43,6 +44,7 @@ lib.mt_linear_fwd.argtypes = [_P, _P, _P, _P, _vp]
 lib.mt_linear_bwd.argtypes = [_P, _P, _P, _P, _P, _P, _u32, _vp, _sz, _vp]
 lib.mt_linear_bwd_workspace.argtypes = [_P, _P, _P, _P, _P, _P, ctypes.POINTER(_sz)]
 lib.mt_matmul.argtypes = [_P, _P, _P, _u32, _vp, _sz, _vp]
+lib.mt_matmul_workspace.argtypes = [_P, _P, _P, _u32, ctypes.POINTER(_sz)]
 lib.mt_reduce_broadcast_grad.argtypes = [_P, _P, _u32, _vp, _sz, _vp]
 lib.mt_reduce_broadcast_grad_workspace.argtypes = [_P, _P, ctypes.POINTER(_sz)]
 lib.mt_broadcast_shape.argtypes = [ctypes.c_int32, _I64P, ctypes.c_int32, _I64P,
@@ -53,7 +55,7 @@ lib.mt_status_str.argtypes = [ctypes.c_int]
 lib.mt_status_str.restype = ctypes.c_char_p
 lib.mt_last_error.argtypes = []
 lib.mt_last_error.restype = ctypes.c_char_p
-for _f in ("mt_linear_fwd", "mt_linear_bwd", "mt_linear_bwd_workspace", "mt_matmul",
+for _f in ("mt_linear_fwd", "mt_linear_bwd", "mt_linear_bwd_workspace", "mt_matmul", "mt_matmul_workspace",
            "mt_reduce_broadcast_grad", "mt_reduce_broadcast_grad_workspace", "mt_broadcast_shape",
            "mt_matmul_shape", "mt_debug_set"):
     getattr(lib, _f).restype = ctypes.c_int
@@ -143,11 +145,20 @@ def linear_bwd(x, w, dy, dx=None, dw=None, db=None, accumulate=False, workspace=
                              _stream(stream)), "mt_linear_bwd")
 
 
-def matmul(a, b, c, accumulate=False, reduce_into=False, stream=None) -> None:
+def matmul_workspace(a, b, c, accumulate=False, reduce_into=False) -> int:
+    flags = (ACCUMULATE if accumulate else 0) | (REDUCE_INTO if reduce_into else 0)
+    n = _sz(0)
+    _check(lib.mt_matmul_workspace(_ref(desc(a)), _ref(desc(b)), _ref(desc(c)), flags,
+                                   ctypes.byref(n)), "mt_matmul_workspace")
+    return int(n.value)
+
+
+def matmul(a, b, c, accumulate=False, reduce_into=False, workspace=None, stream=None) -> None:
     """c = a @ b with broadcasting (c summed over broadcast axes with reduce_into)."""
     flags = (ACCUMULATE if accumulate else 0) | (REDUCE_INTO if reduce_into else 0)
     da, db_, dc = desc(a), desc(b), desc(c)
-    _check(lib.mt_matmul(_ref(da), _ref(db_), _ref(dc), flags, None, 0, _stream(stream)),
+    ptr, nbytes = _ws(workspace)
+    _check(lib.mt_matmul(_ref(da), _ref(db_), _ref(dc), flags, ptr, nbytes, _stream(stream)),
            "mt_matmul")
 
 

@@ -4,6 +4,7 @@
 
 #include <cstdint>
 #include <cstdlib>
+#include <algorithm>
 #include <cstring>
 #include <string>
 
@@ -84,27 +85,31 @@ mt_status hip_status(hipError_t e) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
-int choose_cfg(int64_t M, int64_t N, int64_t batch) {
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Tile configuration: 128x256 / 256x128 blocks run two per CU (one wave per
+// SIMD each), which hides one block's barrier behind the other's matrix-core
+// work (measured faster than 256x256 on 8192^3). Smaller problems take
+// 128x128 when split-K can fill the chip, else 64x64.
+int choose_cfg(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_split) {
   if (g_force_cfg >= 0) return g_force_cfg;
-  auto tiles = [&](int64_t bm, int64_t bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn) * batch; };
-  // 128x256 / 256x128 blocks run two per CU (one wave per SIMD each), which
-  // hides one block's barrier behind the other's matrix-core work; measured
-  // faster than 256x256 (one block per CU) on 8192^3
+  auto tiles = [&](int64_t bm, int64_t bn) { return cdiv(M, bm) * cdiv(N, bn) * batch; };
   if (tiles(128, 256) >= 512) return N >= M ? mt::kCfg128x256 : mt::kCfg256x128;
-  if (tiles(128, 128) >= 128) return mt::kCfg128x128;
+  const int64_t t128 = tiles(128, 128);
+  if (t128 >= 128) return mt::kCfg128x128;
+  if (can_split && t128 * std::min<int64_t>(16, stages / 8) >= 256) return mt::kCfg128x128;
   return mt::kCfg64x64;
 }
 
-// Split-K count for an un-batched product whose tile grid under-fills the chip.
-int choose_splits(int64_t M, int64_t N, int64_t K, int cfg) {
-  if (g_force_splits > 0) return g_force_splits;
-  const int64_t tiles = ((M + mt::gemm_tile_m(cfg) - 1) / mt::gemm_tile_m(cfg)) *
-                        ((N + mt::gemm_tile_n(cfg) - 1) / mt::gemm_tile_n(cfg));
-  if (tiles >= 192) return 1;
-  int64_t s = 256 / (tiles > 0 ? tiles : 1);
-  const int64_t kmax = K / 512;  // keep at least 512 of K per slice
-  if (s > kmax) s = kmax;
-  if (s > 16) s = 16;
+// Split-K runs for a grid of `blocks` tiles over `stages` K-stages: below
+// two blocks per CU, aim for ~512 blocks in all, with at least 8 stages per
+// run and at most 16 runs.
+int choose_splits(int64_t blocks, int64_t stages) {
+  if (g_force_splits > 0) return (int)std::min<int64_t>(g_force_splits, std::max<int64_t>(stages, 1));
+  if (blocks >= 512) return 1;
+  int64_t s = cdiv(512, blocks);
+  s = std::min<int64_t>(s, stages / 8);
+  s = std::min<int64_t>(s, 16);
   return s < 1 ? 1 : (int)s;
 }
 
@@ -138,44 +143,61 @@ bool vec_ok_operand(const void* base, int64_t rows_other, int64_t contig_extent,
 
 int vec_elems(bool bf16) { return bf16 ? 8 : 4; }
 
-mt_status launch_gemm(GemmCall& g, hipStream_t stream, void* ws, size_t ws_bytes) {
+// Resolves the tile configuration, vector width and split-K of a product.
+// Returns the workspace bytes the split needs (0 = no split). With
+// ws_bytes < that, the product runs unsplit.
+size_t plan_gemm(GemmCall& g, bool may_split) {
   mt::GemmParams& p = g.p;
-  if (p.M == 0 || p.N == 0 || p.keep_count == 0) return MT_OK;
-  if (g.cfg < 0) g.cfg = choose_cfg(p.M, p.N, p.keep_count);
   if (g_force_vec1) g.vec = false;
+  const int64_t stages_guess = cdiv(p.K, g.bf16 ? 32 : 16) * p.red_count;
+  if (g.cfg < 0) g.cfg = choose_cfg(p.M, p.N, p.keep_count, stages_guess, may_split);
   // the element-load kernels keep their staging registers within budget up to 128x128
   if (!g.vec && (g.cfg == mt::kCfg256x256 || g.cfg == mt::kCfg256x128 || g.cfg == mt::kCfg128x256))
     g.cfg = mt::kCfg128x128;
+  const int64_t stages = cdiv(p.K, mt::gemm_tile_k(g.cfg, g.bf16)) * p.red_count;
+  p.splits = 1;
+  p.stages_per_split = stages > 0 ? stages : 1;
+  p.partial = nullptr;
+  p.partial_stride = 0;
+  if (!may_split || p.M == 0 || p.N == 0 || p.keep_count == 0 || stages == 0) return 0;
+  const int64_t blocks = cdiv(p.M, mt::gemm_tile_m(g.cfg)) * cdiv(p.N, mt::gemm_tile_n(g.cfg)) *
+                         p.keep_count;
+  const int want = choose_splits(blocks, stages);
+  if (want <= 1) return 0;
+  const int64_t per = cdiv(stages, want);
+  const int64_t splits = cdiv(stages, per);
+  if (splits <= 1) return 0;
+  p.splits = (int32_t)splits;
+  p.stages_per_split = per;
+  p.partial_stride = p.keep_count * p.M * p.N;
+  return (size_t)splits * p.partial_stride * sizeof(float);
+}
+
+mt_status launch_gemm(GemmCall& g, hipStream_t stream, void* ws, size_t ws_bytes) {
+  mt::GemmParams& p = g.p;
+  if (p.M == 0 || p.N == 0 || p.keep_count == 0) return MT_OK;
+  const size_t need = plan_gemm(g, ws != nullptr);
+  if (need > 0 && need <= ws_bytes) {
+    p.partial = (float*)ws;
+  } else {
+    p.splits = 1;
+    const int64_t stages = cdiv(p.K, mt::gemm_tile_k(g.cfg, g.bf16)) * p.red_count;
+    p.stages_per_split = stages > 0 ? stages : 1;
+  }
   // 32-bit buffer offsets: one tile's rows times the row pitch must stay below 2 GiB
   const int64_t es = g.bf16 ? 2 : 4;
   const int64_t rows_a = g.a_kc ? mt::gemm_tile_m(g.cfg) : mt::gemm_tile_k(g.cfg, g.bf16);
   const int64_t rows_b = g.b_kc ? mt::gemm_tile_n(g.cfg) : mt::gemm_tile_k(g.cfg, g.bf16);
   if (rows_a * p.lda * es >= (int64_t)1 << 31 || rows_b * p.ldb * es >= (int64_t)1 << 31)
     return fail(MT_ERR_LAYOUT, "row pitch too large for 32-bit tile offsets");
-  p.splits = 1;
-  p.k_per_split = p.K > 0 ? p.K : 1;
-  if (ws && p.keep_count == 1 && p.red_count == 1) {
-    const int s = choose_splits(p.M, p.N, p.K, g.cfg);
-    const int64_t bk = mt::gemm_tile_k(g.cfg, g.bf16);
-    if (s > 1) {
-      const int64_t kps = ((p.K + s - 1) / s + bk - 1) / bk * bk;
-      const int splits = (int)((p.K + kps - 1) / kps);
-      const size_t need = (size_t)splits * p.M * p.N * sizeof(float);
-      if (splits > 1 && need <= ws_bytes) {
-        p.splits = splits;
-        p.k_per_split = kps;
-        p.partial = (float*)ws;
-        p.partial_stride = p.M * p.N;
-      }
-    }
-  }
   (void)hipGetLastError();  // clear a stale error so the launch check is ours
   hipError_t e = g.bf16 ? mt::gemm_bf16(p, g.a_kc, g.b_kc, g.vec, g.cfg, stream)
                         : mt::gemm_f32(p, g.a_kc, g.b_kc, g.vec, g.cfg, stream);
   if (e != hipSuccess) return hip_status(e);
   if (p.splits > 1) {
-    e = mt::splitk_finish(p.partial, p.splits, p.M, p.N, p.c, p.ldc, p.bias, p.accumulate != 0,
-                          stream);
+    // batch elements of C are contiguous M x N blocks when batched (mt_matmul)
+    e = mt::splitk_finish(p.partial, p.splits, p.keep_count * p.M, p.N, p.c, p.ldc, p.bias,
+                          p.accumulate != 0, stream);
     if (e != hipSuccess) return hip_status(e);
   }
   return MT_OK;
@@ -259,9 +281,32 @@ mt_status linear_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tenso
   }
   const bool acc = (flags & MT_ACCUMULATE) != 0;
 
-  // workspace needs: dw split-K partials and db row-slice sums (used in turn)
-  size_t need_dw = 0, need_db = 0;
-  GemmCall gdw{};
+  // workspace needs (used in turn on the stream, so the size is the max):
+  // dx / dw split-K partials and db row-slice sums
+  GemmCall gdx{}, gdw{};
+  size_t need_dx = 0, need_dw = 0, need_db = 0;
+  if (dx && M > 0 && K > 0) {
+    init_params(&gdx.p);
+    gdx.p.a = dy->data;
+    gdx.p.b = w->data;
+    gdx.p.c = (float*)dx->data;
+    gdx.p.M = M;
+    gdx.p.N = K;
+    gdx.p.K = N;
+    gdx.p.lda = pitch(dy);
+    gdx.p.ldb = pitch(w);
+    gdx.p.ldc = pitch(dx);
+    gdx.p.accumulate = acc;
+    gdx.a_kc = true;
+    gdx.b_kc = false;
+    gdx.bf16 = bf;
+    gdx.vec = vec_ok_operand(dy->data, M, N, gdx.p.lda, nullptr, 0, per) &&
+              vec_ok_operand(w->data, N, K, gdx.p.ldb, nullptr, 0, per) && aligned16(dx->data) &&
+              K % 4 == 0 && gdx.p.ldc % 4 == 0;
+    gdx.cfg = -1;
+    GemmCall probe = gdx;
+    need_dx = plan_gemm(probe, true);
+  }
   if (dw && N > 0 && K > 0) {
     init_params(&gdw.p);
     gdw.p.a = dy->data;
@@ -280,9 +325,9 @@ mt_status linear_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tenso
     gdw.vec = vec_ok_operand(dy->data, M, N, gdw.p.lda, nullptr, 0, per) &&
               vec_ok_operand(x->data, M, K, gdw.p.ldb, nullptr, 0, per) &&
               aligned16(dw->data) && K % 4 == 0 && gdw.p.ldc % 4 == 0;
-    gdw.cfg = choose_cfg(N, K, 1);
-    const int sp = choose_splits(N, K, M, gdw.cfg);
-    if (sp > 1) need_dw = (size_t)sp * N * K * sizeof(float);
+    gdw.cfg = -1;
+    GemmCall probe = gdw;
+    need_dw = plan_gemm(probe, true);
   }
   int parts = 1;
   if (db && N > 0) {
@@ -290,36 +335,17 @@ mt_status linear_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tenso
     if (parts > 1) need_db = (size_t)parts * N * sizeof(float);
   }
   if (ws_query) {
-    *ws_query = need_dw > need_db ? need_dw : need_db;
+    *ws_query = std::max(need_dx, std::max(need_dw, need_db));
     return MT_OK;
   }
   if (ws && ((uintptr_t)ws & 255))
     return fail(MT_ERR_WORKSPACE, "workspace must be 256-byte aligned");
 
   if (dx && M > 0 && K > 0) {
-    GemmCall g{};
-    init_params(&g.p);
-    g.p.a = dy->data;
-    g.p.b = w->data;
-    g.p.c = (float*)dx->data;
-    g.p.M = M;
-    g.p.N = K;
-    g.p.K = N;
-    g.p.lda = pitch(dy);
-    g.p.ldb = pitch(w);
-    g.p.ldc = pitch(dx);
-    g.p.accumulate = acc;
-    g.a_kc = true;
-    g.b_kc = false;
-    g.bf16 = bf;
-    g.vec = vec_ok_operand(dy->data, M, N, g.p.lda, nullptr, 0, per) &&
-            vec_ok_operand(w->data, N, K, g.p.ldb, nullptr, 0, per) && aligned16(dx->data) &&
-            K % 4 == 0 && g.p.ldc % 4 == 0;
-    g.cfg = -1;
-    if ((s = launch_gemm(g, stream, nullptr, 0))) return s;
+    if ((s = launch_gemm(gdx, stream, ws, ws_bytes))) return s;
   }
   if (dw && N > 0 && K > 0) {
-    if ((s = launch_gemm(gdw, stream, ws, ws && ws_bytes >= need_dw ? ws_bytes : 0))) return s;
+    if ((s = launch_gemm(gdw, stream, ws, ws_bytes))) return s;
   }
   if (db && N > 0) {
     (void)hipGetLastError();
@@ -332,7 +358,7 @@ mt_status linear_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tenso
 }
 
 mt_status matmul_impl(const mt_tensor* a, const mt_tensor* b, const mt_tensor* c, uint32_t flags,
-                      hipStream_t stream) {
+                      void* ws, size_t ws_bytes, hipStream_t stream, size_t* ws_query) {
   if (flags & ~(MT_ACCUMULATE | MT_REDUCE_INTO)) return fail(MT_ERR_INVALID, "mt_matmul: unknown flags");
   mt_status s;
   if ((s = check_tensor(a, "a", 1, MT_MAX_DIMS))) return s;
@@ -387,7 +413,10 @@ mt_status matmul_impl(const mt_tensor* a, const mt_tensor* b, const mt_tensor* c
   if (overlaps(c, a) || overlaps(c, b)) return fail(MT_ERR_ALIAS, "c overlaps an input");
   for (int i = 0; i < p.nkeep; ++i) p.keep_count *= p.keep_shape[i];
   for (int i = 0; i < p.nred; ++i) p.red_count *= p.red_shape[i];
-  if (pl.M == 0 || pl.N == 0 || p.keep_count == 0) return MT_OK;
+  if (pl.M == 0 || pl.N == 0 || p.keep_count == 0) {
+    if (ws_query) *ws_query = 0;
+    return MT_OK;
+  }
   GemmCall g{};
   g.p = p;
   bool a_kc, b_kc;
@@ -419,7 +448,13 @@ mt_status matmul_impl(const mt_tensor* a, const mt_tensor* b, const mt_tensor* c
           vec_ok_operand(b->data, b_kc ? pl.N : pl.K, b_kc ? pl.K : pl.N, ldb, sb_all, na, per) &&
           aligned16(c->data) && pl.N % 4 == 0;
   g.cfg = -1;
-  return launch_gemm(g, stream, nullptr, 0);
+  if (ws_query) {
+    GemmCall probe = g;
+    *ws_query = plan_gemm(probe, true);
+    return MT_OK;
+  }
+  if (ws && ((uintptr_t)ws & 255)) return fail(MT_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  return launch_gemm(g, stream, ws, ws_bytes);
 }
 
 mt_status reduce_impl(const mt_tensor* go, const mt_tensor* gi, uint32_t flags, void* ws,
@@ -519,9 +554,17 @@ mt_status mt_linear_bwd_workspace(const mt_tensor* x, const mt_tensor* w, const 
 mt_status mt_matmul(const mt_tensor* a, const mt_tensor* b, const mt_tensor* c, uint32_t flags,
                     void* ws, size_t ws_bytes, void* stream) {
   try {
-    (void)ws;
-    (void)ws_bytes;
-    return matmul_impl(a, b, c, flags, (hipStream_t)stream);
+    return matmul_impl(a, b, c, flags, ws, ws_bytes, (hipStream_t)stream, nullptr);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_matmul_workspace(const mt_tensor* a, const mt_tensor* b, const mt_tensor* c,
+                              uint32_t flags, size_t* bytes) {
+  try {
+    if (!bytes) return fail(MT_ERR_NULL, "bytes is null");
+    return matmul_impl(a, b, c, flags, nullptr, 0, nullptr, bytes);
   } catch (...) {
     return fail(MT_ERR_INVALID, "internal error");
   }

@@ -269,18 +269,20 @@ void gemm_kernel(const GemmParams p) {
   const char* A = (const char*)p.a + a_off * ES;
   const char* B = (const char*)p.b + b_off * ES;
 
-  const int64_t k_begin = (int64_t)split * p.k_per_split;
-  const int64_t k_end = (k_begin + p.k_per_split) < p.K ? (k_begin + p.k_per_split) : p.K;
-  const int64_t KS = k_end > k_begin ? (k_end - k_begin + BK - 1) / BK : 0;
-  const int64_t S = KS * p.red_count;
+  const int64_t KS = (p.K + BK - 1) / BK;  // k tiles per summed batch index
+  const int64_t S_all = KS * p.red_count;
+  const int64_t st0 = (int64_t)split * p.stages_per_split;
+  const int64_t st1 = (st0 + p.stages_per_split) < S_all ? (st0 + p.stages_per_split) : S_all;
+  const int64_t S = st1 > st0 ? st1 - st0 : 0;
 
   TA ta;
   TB tb;
   ta.init(tid, p.lda);
   tb.init(tid, p.ldb);
 
-  // stage cursor (reduction index r, k tile kt) with r's operand offsets
-  int64_t cur_r = 0, cur_kt = 0, ra_off = 0, rb_off = 0;
+  // stage cursor (summed batch index r, k tile kt) with r's operand offsets
+  int64_t cur_r = KS > 0 ? st0 / KS : 0, cur_kt = KS > 0 ? st0 % KS : 0;
+  int64_t ra_off = 0, rb_off = 0;
   auto red_offsets = [&](int64_t r) {
     ra_off = 0;
     rb_off = 0;
@@ -292,13 +294,13 @@ void gemm_kernel(const GemmParams p) {
     }
   };
   auto load_stage = [&]() {
-    const int64_t k0 = k_begin + cur_kt * BK;
+    const int64_t k0 = cur_kt * BK;
     const char* Ar = A + ra_off * ES;
     const char* Br = B + rb_off * ES;
-    if (A_KC) ta.load(Ar + (m0 * p.lda + k0) * ES, p.M - m0, k_end - k0);
-    else ta.load(Ar + (k0 * p.lda + m0) * ES, k_end - k0, p.M - m0);
-    if (B_KC) tb.load(Br + (n0 * p.ldb + k0) * ES, p.N - n0, k_end - k0);
-    else tb.load(Br + (k0 * p.ldb + n0) * ES, k_end - k0, p.N - n0);
+    if (A_KC) ta.load(Ar + (m0 * p.lda + k0) * ES, p.M - m0, p.K - k0);
+    else ta.load(Ar + (k0 * p.lda + m0) * ES, p.K - k0, p.M - m0);
+    if (B_KC) tb.load(Br + (n0 * p.ldb + k0) * ES, p.N - n0, p.K - k0);
+    else tb.load(Br + (k0 * p.ldb + n0) * ES, p.K - k0, p.N - n0);
   };
   auto advance = [&]() {
     if (++cur_kt == KS) {
@@ -315,7 +317,7 @@ void gemm_kernel(const GemmParams p) {
     for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
 
   if (S > 0) {
-    if (p.nred > 0) red_offsets(0);
+    if (p.nred > 0) red_offsets(cur_r);
     load_stage();
     advance();
     ta.store(lds);
@@ -343,7 +345,8 @@ void gemm_kernel(const GemmParams p) {
 
   // ---- epilogue: lane holds C[m][n0' + 8g + 4h + 0..3] in acc regs 4g..4g+3
   const bool to_partial = p.splits > 1;
-  float* C = to_partial ? p.partial + (int64_t)split * p.partial_stride : p.c + c_off;
+  float* C = to_partial ? p.partial + (int64_t)split * p.partial_stride + batch * p.M * p.N
+                        : p.c + c_off;
   const int64_t ldc = to_partial ? p.N : p.ldc;
   constexpr bool VEC_C = VEC > 1;  // host guarantees N % 4 == 0 and aligned C / bias then
 #pragma unroll

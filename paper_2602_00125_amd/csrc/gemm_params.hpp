@@ -35,10 +35,13 @@ struct GemmParams {
   int32_t tiles_m, tiles_n;
   int32_t accumulate;  // C += result
   int32_t group_m;     // tile-order group height (L2 reuse)
-  // split-K: the k range is cut into `splits` slices; slice s of block writes
-  // its partial tile to `partial + s * partial_stride` (row-major, pitch N)
+  // split-K: the sequence of K-stages (every summed batch index r times every
+  // BK-wide k tile, r outermost) is cut into `splits` runs of
+  // `stages_per_split` stages; run s writes its partial tile of batch
+  // element beta to partial + s * partial_stride + beta * M * N (row-major,
+  // pitch N), and a second pass adds the runs in order
   int32_t splits;
-  int64_t k_per_split;   // multiple of the kernel's BK
+  int64_t stages_per_split;
   float* partial;
   int64_t partial_stride;
 };

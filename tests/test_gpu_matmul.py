@@ -16,19 +16,23 @@ b = pytest.importorskip("paper_2602_00125_amd.binding")
 DEV = "cuda:0"
 
 
-def gpu_matmul(a, c_shape, bb, accumulate=False, reduce_into=False, prior=None):
+def gpu_matmul(a, c_shape, bb, accumulate=False, reduce_into=False, prior=None, use_ws=True):
     out = torch.full(c_shape, float("nan"), device=DEV)
     if prior is not None:
         out.copy_(prior)
-    b.matmul(a, bb, out, accumulate=accumulate, reduce_into=reduce_into)
+    ws = None
+    if use_ws:
+        n = b.matmul_workspace(a, bb, out, accumulate=accumulate, reduce_into=reduce_into)
+        ws = torch.empty(n // 4 + 64, device=DEV) if n else None
+    b.matmul(a, bb, out, accumulate=accumulate, reduce_into=reduce_into, workspace=ws)
     torch.cuda.synchronize()
     return out
 
 
-def bmm_grads_folded(A, B, dC):
+def bmm_grads_folded(A, B, dC, use_ws=True):
     """dA, dB by folding the broadcast-axis sums into the products."""
-    dA = gpu_matmul(dC, A.shape, B.transpose(-1, -2), reduce_into=True)
-    dB = gpu_matmul(A.transpose(-1, -2), B.shape, dC, reduce_into=True)
+    dA = gpu_matmul(dC, A.shape, B.transpose(-1, -2), reduce_into=True, use_ws=use_ws)
+    dB = gpu_matmul(A.transpose(-1, -2), B.shape, dC, reduce_into=True, use_ws=use_ws)
     return dA, dB
 
 
@@ -59,6 +63,19 @@ def test_bmm_broadcast_16x1x509x257_by_1x8x257x383():
     # deterministic reruns
     dA_again, dB_again = bmm_grads_folded(A, B, dC)
     assert torch.equal(dA, dA_again) and torch.equal(dB, dB_again)
+    # without workspace (no split-K): the same bar
+    dA3, dB3 = bmm_grads_folded(A, B, dC, use_ws=False)
+    assert_close(to_f64(dA3), dAr, SA, what="dA (folded, unsplit)")
+    assert_close(to_f64(dB3), dBr, SB, what="dB (folded, unsplit)")
+    # forced split counts, including splits that cut a summed batch index
+    for splits in (2, 3, 7):
+        b.debug_set("splits", splits)
+        try:
+            dA4, dB4 = bmm_grads_folded(A, B, dC)
+        finally:
+            b.debug_set("splits", 0)
+        assert_close(to_f64(dA4), dAr, SA, what=f"dA (splits={splits})")
+        assert_close(to_f64(dB4), dBr, SB, what=f"dB (splits={splits})")
 
 
 def _rand_case(rng):
@@ -99,7 +116,7 @@ def test_bmm_random_broadcast_shapes(seed):
     Cr, SC = oracle.matmul(A.double().numpy(), B.double().numpy())
     assert_close(to_f64(C), Cr, SC, what=f"C {ashape}@{bshape}")
     if len(ashape) >= 2 and len(bshape) >= 2:
-        dA, dB = bmm_grads_folded(Ad, Bd, dC.to(DEV))
+        dA, dB = bmm_grads_folded(Ad, Bd, dC.to(DEV), use_ws=bool(seed % 2))
         dAr, SA, dBr, SB = oracle.matmul_bwd(A.double().numpy(), B.double().numpy(), dC.double().numpy())
         assert_close(to_f64(dA), dAr, SA, what="dA")
         assert_close(to_f64(dB), dBr, SB, what="dB")
