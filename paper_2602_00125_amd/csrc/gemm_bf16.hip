@@ -15,20 +15,25 @@ static hipError_t launch_bf16(const GemmParams& p, hipStream_t stream) {
   if (blocks <= 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL((gemm::gemm_kernel<__bf16, A_KC, B_KC, BM, BN, BK, WGM, WGN, VEC, WPE>),
-                     dim3((unsigned)blocks), dim3(256), 0, stream, q);
+                     dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
   return hipGetLastError();
 }
 
 template <bool A_KC, bool B_KC, int VEC>
 static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream) {
-  // element-load kernels exist up to 128x128 (larger tiles would spill staging registers)
-  if (VEC == 1 && cfg != kCfg64x64) cfg = kCfg128x128;
-  switch (cfg) {
-    case kCfg256x256: return launch_bf16<A_KC, B_KC, 256, 256, 32, 2, 2, VEC, 1>(p, stream);
-    case kCfg256x128: return launch_bf16<A_KC, B_KC, 256, 128, 32, 2, 2, VEC, 2>(p, stream);
-    case kCfg128x256: return launch_bf16<A_KC, B_KC, 128, 256, 32, 2, 2, VEC, 2>(p, stream);
-    case kCfg128x128: return launch_bf16<A_KC, B_KC, 128, 128, 32, 2, 2, VEC, 2>(p, stream);
-    default: return launch_bf16<A_KC, B_KC, 64, 64, 32, 2, 2, VEC, 4>(p, stream);
+  if constexpr (VEC == 1) {
+    // element-load kernels exist up to 128x128 (larger tiles would spill staging registers)
+    if (cfg == kCfg64x64) return launch_bf16<A_KC, B_KC, 64, 64, 32, 2, 2, 1, 4>(p, stream);
+    return launch_bf16<A_KC, B_KC, 128, 128, 32, 2, 2, 1, 2>(p, stream);
+  } else {
+    switch (cfg) {
+      case kCfg256x256: return launch_bf16<A_KC, B_KC, 256, 256, 32, 2, 2, VEC, 1>(p, stream);
+      case kCfg256x256x64w8: return launch_bf16<A_KC, B_KC, 256, 256, 64, 2, 4, VEC, 2>(p, stream);
+      case kCfg256x128: return launch_bf16<A_KC, B_KC, 256, 128, 32, 2, 2, VEC, 2>(p, stream);
+      case kCfg128x256: return launch_bf16<A_KC, B_KC, 128, 256, 32, 2, 2, VEC, 2>(p, stream);
+      case kCfg128x128: return launch_bf16<A_KC, B_KC, 128, 128, 32, 2, 2, VEC, 2>(p, stream);
+      default: return launch_bf16<A_KC, B_KC, 64, 64, 32, 2, 2, VEC, 4>(p, stream);
+    }
   }
 }
 

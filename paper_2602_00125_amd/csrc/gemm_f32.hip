@@ -14,38 +14,46 @@ static hipError_t launch_f32(const GemmParams& p, hipStream_t stream) {
   if (blocks <= 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL((gemm::gemm_kernel<float, A_KC, B_KC, BM, BN, BK, WGM, WGN, VEC, WPE>),
-                     dim3((unsigned)blocks), dim3(256), 0, stream, q);
+                     dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
   return hipGetLastError();
 }
 
 template <bool A_KC, bool B_KC, int VEC>
 static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream) {
-  // element-load kernels exist up to 128x128 (larger tiles would spill staging registers)
-  if (VEC == 1 && cfg != kCfg64x64) cfg = kCfg128x128;
-  switch (cfg) {
-    case kCfg256x256: return launch_f32<A_KC, B_KC, 256, 256, 16, 2, 2, VEC, 1>(p, stream);
-    case kCfg256x128: return launch_f32<A_KC, B_KC, 256, 128, 16, 2, 2, VEC, 2>(p, stream);
-    case kCfg128x256: return launch_f32<A_KC, B_KC, 128, 256, 16, 2, 2, VEC, 2>(p, stream);
-    case kCfg128x128: return launch_f32<A_KC, B_KC, 128, 128, 16, 2, 2, VEC, 2>(p, stream);
-    default: return launch_f32<A_KC, B_KC, 64, 64, 16, 2, 2, VEC, 4>(p, stream);
+  if constexpr (VEC == 1) {
+    // element-load kernels exist up to 128x128 (larger tiles would spill staging registers)
+    if (cfg == kCfg64x64) return launch_f32<A_KC, B_KC, 64, 64, 16, 2, 2, 1, 4>(p, stream);
+    return launch_f32<A_KC, B_KC, 128, 128, 16, 2, 2, 1, 2>(p, stream);
+  } else {
+    switch (cfg) {
+      case kCfg256x256:
+      case kCfg256x256x64w8: return launch_f32<A_KC, B_KC, 256, 256, 16, 2, 2, VEC, 1>(p, stream);
+      case kCfg256x128: return launch_f32<A_KC, B_KC, 256, 128, 16, 2, 2, VEC, 2>(p, stream);
+      case kCfg128x256: return launch_f32<A_KC, B_KC, 128, 256, 16, 2, 2, VEC, 2>(p, stream);
+      case kCfg128x128: return launch_f32<A_KC, B_KC, 128, 128, 16, 2, 2, VEC, 2>(p, stream);
+      default: return launch_f32<A_KC, B_KC, 64, 64, 16, 2, 2, VEC, 4>(p, stream);
+    }
   }
 }
 
 int gemm_tile_m(int cfg) {
   switch (cfg) {
-    case kCfg256x256: case kCfg256x128: return 256;
+    case kCfg256x256: case kCfg256x128: case kCfg256x256x64w8: return 256;
     case kCfg128x256: case kCfg128x128: return 128;
     default: return 64;
   }
 }
 int gemm_tile_n(int cfg) {
   switch (cfg) {
-    case kCfg256x256: case kCfg128x256: return 256;
+    case kCfg256x256: case kCfg128x256: case kCfg256x256x64w8: return 256;
     case kCfg256x128: case kCfg128x128: return 128;
     default: return 64;
   }
 }
-int gemm_tile_k(int, bool bf16) { return bf16 ? 32 : 16; }
+int gemm_tile_k(int cfg, bool bf16) {
+  if (cfg == kCfg256x256x64w8) return bf16 ? 64 : 16;
+  return bf16 ? 32 : 16;
+}
 
 hipError_t gemm_f32(const GemmParams& p, bool a_kc, bool b_kc, bool vec, int cfg,
                     hipStream_t stream) {

@@ -9,7 +9,7 @@
 // covers Y = X W^T (both K-contiguous), dX = dY W (A K-contiguous, B
 // N-contiguous) and dW = dY^T X (both M/N-contiguous).
 //
-// Block: 256 threads = 4 wave64s in a WGM x WGN grid; each wave owns a
+// Block: 4 or 8 wave64s in a WGM x WGN grid; each wave owns a
 // (BM/WGM) x (BN/WGN) sub-tile made of 32x32 MFMA tiles held in accumulator
 // registers. Per K-stage of BK:
 //   global -> registers (16-byte buffer_load_dwordx4; out-of-range rows and
@@ -25,8 +25,8 @@
 // fp32: within a group of 8 k, MFMA step j (0..3) takes k = 8g + 4h + j for
 // lane half h on both operands, so one ds_read_b128 feeds 4 steps.
 // bf16: one MFMA step covers 16 k; lane half h supplies k = 16s + 8h + 0..7
-// (one ds_read_b128 from a K-contiguous tile, eight 16-bit reads from an
-// M/N-contiguous one).
+// (one ds_read_b128 from a K-contiguous tile, two transposing
+// ds_read_b64_tr_b16 from an M/N-contiguous one).
 // The MFMA's row operand is the B tile (n) and its column operand the A tile
 // (m): each lane then holds 4 consecutive n of one output row per register
 // quad, which the epilogue stores with one 16-byte store (bias added there).
@@ -80,16 +80,20 @@ struct Chunk<2> {
 
 // One operand's BMN x BK tile: global -> registers -> LDS. Sizes in elements
 // of ESIZE bytes; LDS addressed in bytes.
-template <int ESIZE, bool KC, int BMN, int BK, int VEC>
+template <int ESIZE, bool KC, int BMN, int BK, int VEC, int NT>
 struct Tile {
-  static constexpr int PAD = KC ? 16 / ESIZE : 8;          // elements
+  // K-contiguous rows: +16 bytes (an odd multiple of 16 bytes between rows
+  // keeps 16-byte reads of consecutive rows conflict-free). M/N-contiguous
+  // rows: fp32 +8 elements; bf16 +16 elements, so that the 4 rows read by a
+  // 16-lane group of ds_read_b64_tr_b16 start 32 bytes apart modulo 128.
+  static constexpr int PAD = KC ? 16 / ESIZE : (ESIZE == 2 ? 16 : 8);  // elements
   static constexpr int PITCH = (KC ? BK : BMN) + PAD;       // elements per LDS row
   static constexpr int ROWS = KC ? BMN : BK;
   static constexpr int COLS = KC ? BK : BMN;                // contiguous extent
   static constexpr int BYTES = ROWS * PITCH * ESIZE;        // per stage
   static constexpr int VPR = COLS / VEC;                    // chunks per row
-  static constexpr int PER_THREAD = ROWS * VPR / 256;
-  static_assert((ROWS * VPR) % 256 == 0, "tile must split evenly over 256 threads");
+  static constexpr int PER_THREAD = ROWS * VPR / NT;
+  static_assert((ROWS * VPR) % NT == 0, "tile must split evenly over the block's threads");
   static_assert((PITCH * ESIZE) % 16 == 0, "LDS rows stay 16-byte aligned");
   using C = Chunk<VEC * ESIZE>;
   using V = typename C::T;
@@ -101,7 +105,7 @@ struct Tile {
   __device__ __forceinline__ void init(int tid, int64_t ld) {
 #pragma unroll
     for (int i = 0; i < PER_THREAD; ++i) {
-      const int c = tid + i * 256;
+      const int c = tid + i * NT;
       row[i] = c / VPR;
       col[i] = (c % VPR) * VEC;
       off[i] = (uint32_t)(((int64_t)row[i] * ld + col[i]) * ESIZE);
@@ -185,25 +189,47 @@ struct Mma<float, A_KC, B_KC, TM, TN, BK, PA, PB> {
 
 template <bool A_KC, bool B_KC, int TM, int TN, int BK, int PA, int PB>
 struct Mma<__bf16, A_KC, B_KC, TM, TN, BK, PA, PB> {
-  static __device__ __forceinline__ u16x8 frag(const unsigned short* S, bool kc, int P, int mn,
-                                               int k0) {
-    if (kc) return *(const u16x8*)&S[mn * P + k0];
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  // 8 consecutive k (k0 .. k0+7) of row/column mn for this lane.
+  // K-contiguous tile [mn][k]: one 16-byte read.
+  // M/N-contiguous tile [k][mn]: two ds_read_b64_tr_b16. Within each group of
+  // 16 lanes, lane i of the group receives element i % 4 of the 8-byte
+  // chunks addressed by lanes i/4, 4 + i/4, 8 + i/4, 12 + i/4 of the group.
+  // Lane s of a group therefore addresses row k + s/4, columns
+  // c0 + 4 (s % 4) .. +3, where c0 is the group's first column, and lane i
+  // receives column c0 + i at rows k .. k+3.
+  static __device__ __forceinline__ u16x8 frag_kc(const unsigned short* S, int P, int mn, int k0) {
+    return *(const u16x8*)&S[mn * P + k0];
+  }
+  static __device__ __forceinline__ u16x8 frag_mc(const unsigned short* S, int P, int col0, int k0,
+                                                  int lane) {
+    const int g = lane >> 4, s = lane & 15;
+    const int row = k0 + (s >> 2);
+    const int col = col0 + 16 * (g & 1) + 4 * (s & 3);
+    const unsigned short* p0 = &S[row * P + col];
+    const unsigned short* p1 = p0 + 4 * P;
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(const void*)p0);
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(const void*)p1);
     u16x8 v;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = S[(k0 + e) * P + mn];
+    v[0] = lo[0]; v[1] = lo[1]; v[2] = lo[2]; v[3] = lo[3];
+    v[4] = hi[0]; v[5] = hi[1]; v[6] = hi[2]; v[7] = hi[3];
     return v;
   }
   static __device__ __forceinline__ void run(const unsigned short* As, const unsigned short* Bs,
                                              int am, int bn, int l32, int h,
                                              f32x16 (&acc)[TM][TN]) {
+    const int lane = l32 + 32 * h;
 #pragma unroll
     for (int s = 0; s < BK / 16; ++s) {
       const int k0 = 16 * s + 8 * h;
       u16x8 af[TM], bf[TN];
 #pragma unroll
-      for (int i = 0; i < TM; ++i) af[i] = frag(As, A_KC, PA, am + i * 32 + l32, k0);
+      for (int i = 0; i < TM; ++i)
+        af[i] = A_KC ? frag_kc(As, PA, am + i * 32 + l32, k0) : frag_mc(As, PA, am + i * 32, k0, lane);
 #pragma unroll
-      for (int i = 0; i < TN; ++i) bf[i] = frag(Bs, B_KC, PB, bn + i * 32 + l32, k0);
+      for (int i = 0; i < TN; ++i)
+        bf[i] = B_KC ? frag_kc(Bs, PB, bn + i * 32 + l32, k0) : frag_mc(Bs, PB, bn + i * 32, k0, lane);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -220,15 +246,17 @@ template <> struct LdsElem<__bf16> { using type = unsigned short; };
 
 template <typename T, bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int WGN, int VEC,
           int WAVES_PER_EU>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
+__global__ __launch_bounds__(WGM * WGN * 64)
+__attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
 void gemm_kernel(const GemmParams p) {
   constexpr int ES = (int)sizeof(T);
+  constexpr int NT = WGM * WGN * 64;  // threads per block
   constexpr int WTM = BM / WGM, WTN = BN / WGN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
-  static_assert(WGM * WGN == 4, "4 waves per block");
+  static_assert(WGM * WGN == 4 || WGM * WGN == 8, "4 or 8 waves per block");
   static_assert(TM * 32 == WTM && TN * 32 == WTN && BK % 16 == 0, "tile shape");
-  using TA = Tile<ES, A_KC, BM, BK, VEC>;
-  using TB = Tile<ES, B_KC, BN, BK, VEC>;
+  using TA = Tile<ES, A_KC, BM, BK, VEC, NT>;
+  using TB = Tile<ES, B_KC, BN, BK, VEC, NT>;
   using E = typename LdsElem<T>::type;
   __shared__ __attribute__((aligned(16))) char lds[2 * (TA::BYTES + TB::BYTES)];
 

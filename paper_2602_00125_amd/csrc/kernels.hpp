@@ -8,8 +8,17 @@
 
 namespace mt {
 
-// GEMM tile configurations (BM x BN; BK = 16; 4 waves per block).
-enum GemmCfg { kCfg256x256 = 0, kCfg256x128 = 1, kCfg128x256 = 2, kCfg128x128 = 3, kCfg64x64 = 4 };
+// GEMM tile configurations (BM x BN; BK = 16 fp32 / 32 bf16; 4 waves per
+// block), plus a bf16 256x256 configuration with BK = 64 and 8 waves (fp32
+// runs it as 256x256).
+enum GemmCfg {
+  kCfg256x256 = 0,
+  kCfg256x128 = 1,
+  kCfg128x256 = 2,
+  kCfg128x128 = 3,
+  kCfg64x64 = 4,
+  kCfg256x256x64w8 = 5
+};
 int gemm_tile_m(int cfg);
 int gemm_tile_n(int cfg);
 int gemm_tile_k(int cfg, bool bf16);
