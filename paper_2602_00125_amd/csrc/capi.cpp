@@ -91,13 +91,17 @@ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // SIMD each), which hides one block's barrier behind the other's matrix-core
 // work (measured faster than 256x256 on 8192^3). Smaller problems take
 // 128x128 when split-K can fill the chip, else 64x64.
-int choose_cfg(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_split, bool bf16) {
+int choose_cfg(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_split, bool bf16,
+               bool both_kc) {
   if (g_force_cfg >= 0) return g_force_cfg;
   auto tiles = [&](int64_t bm, int64_t bn) { return cdiv(M, bm) * cdiv(N, bn) * batch; };
   // bf16 moves half the bytes per flop of fp32 at 16x the matrix rate, so
   // large bf16 products need the bigger 256x256 tile (twice the flops per
-  // loaded byte of 128x256) with 8 waves and BK = 64
-  if (bf16 && tiles(256, 256) >= 256) return mt::kCfg256x256x64w8;
+  // loaded byte of 128x256) with 8 waves and BK = 64. For fp32 the 8-wave
+  // 256x256 tile (BK = 32) measured faster only when both operands are
+  // K-contiguous (Y = X W^T), whose 64-byte row segments per BK = 16 stage
+  // otherwise fetch half cache lines.
+  if (tiles(256, 256) >= 256 && (bf16 || both_kc)) return mt::kCfg256x256x64w8;
   if (tiles(128, 256) >= 512) return N >= M ? mt::kCfg128x256 : mt::kCfg256x128;
   const int64_t t128 = tiles(128, 128);
   if (t128 >= 128) return mt::kCfg128x128;
@@ -154,7 +158,8 @@ size_t plan_gemm(GemmCall& g, bool may_split) {
   mt::GemmParams& p = g.p;
   if (g_force_vec1) g.vec = false;
   const int64_t stages_guess = cdiv(p.K, g.bf16 ? 32 : 16) * p.red_count;
-  if (g.cfg < 0) g.cfg = choose_cfg(p.M, p.N, p.keep_count, stages_guess, may_split, g.bf16);
+  if (g.cfg < 0)
+    g.cfg = choose_cfg(p.M, p.N, p.keep_count, stages_guess, may_split, g.bf16, g.a_kc && g.b_kc);
   // the element-load kernels keep their staging registers within budget up to 128x128
   if (!g.vec && g.cfg != mt::kCfg64x64) g.cfg = mt::kCfg128x128;
   const int64_t stages = cdiv(p.K, mt::gemm_tile_k(g.cfg, g.bf16)) * p.red_count;

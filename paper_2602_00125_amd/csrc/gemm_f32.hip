@@ -26,8 +26,8 @@ static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream
     return launch_f32<A_KC, B_KC, 128, 128, 16, 2, 2, 1, 2>(p, stream);
   } else {
     switch (cfg) {
-      case kCfg256x256:
-      case kCfg256x256x64w8: return launch_f32<A_KC, B_KC, 256, 256, 16, 2, 2, VEC, 1>(p, stream);
+      case kCfg256x256: return launch_f32<A_KC, B_KC, 256, 256, 16, 2, 2, VEC, 1>(p, stream);
+      case kCfg256x256x64w8: return launch_f32<A_KC, B_KC, 256, 256, 32, 2, 4, VEC, 2>(p, stream);
       case kCfg256x128: return launch_f32<A_KC, B_KC, 256, 128, 16, 2, 2, VEC, 2>(p, stream);
       case kCfg128x256: return launch_f32<A_KC, B_KC, 128, 256, 16, 2, 2, VEC, 2>(p, stream);
       case kCfg128x128: return launch_f32<A_KC, B_KC, 128, 128, 16, 2, 2, VEC, 2>(p, stream);
@@ -51,7 +51,7 @@ int gemm_tile_n(int cfg) {
   }
 }
 int gemm_tile_k(int cfg, bool bf16) {
-  if (cfg == kCfg256x256x64w8) return bf16 ? 64 : 16;
+  if (cfg == kCfg256x256x64w8) return bf16 ? 64 : 32;
   return bf16 ? 32 : 16;
 }
 

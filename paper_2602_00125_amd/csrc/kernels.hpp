@@ -9,8 +9,8 @@
 namespace mt {
 
 // GEMM tile configurations (BM x BN; BK = 16 fp32 / 32 bf16; 4 waves per
-// block), plus a bf16 256x256 configuration with BK = 64 and 8 waves (fp32
-// runs it as 256x256).
+// block), plus a 256x256 configuration with 8 waves and BK = 32 fp32 / 64
+// bf16.
 enum GemmCfg {
   kCfg256x256 = 0,
   kCfg256x128 = 1,
