@@ -3,9 +3,10 @@
 
 One step = the whole hot path on one batch of synthetic inputs already in
 HBM: Y = X W^T + b (mt_linear_fwd), then dX = dY W, dW = dY^T X and
-db = 1^T dY (mt_linear_bwd, issued one output at a time so that HIP events
-bracket each kernel; the kernels are the ones a single call with all three
-outputs launches, in the same order, on the same stream).
+db = 1^T dY (one mt_linear_bwd call). The step time comes from events
+around the timed steps; a second pass issues the same kernels with the
+backward split into one call per output, so that HIP events bracket each
+kernel for the roofline of the dominant one.
 
 Prints ONE JSON line: TFLOP/s of the three products (6 M N K flop per step)
 over the timed steps, the dominant kernel's roofline, and the fp64 CPU
@@ -118,13 +119,16 @@ def cpu_baseline(inp, seconds: float):
 
 
 def timed_steps(step, n_events: int, steps: int, warmup: int):
-    """Warm up, then time `steps` steps with events between their calls."""
+    """Warm up, then time `steps` steps (events between their calls when
+    n_events > 1); returns (mean ms per step, mean ms between events)."""
     import torch
 
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(n_events)] for _ in range(steps)]
+    if n_events < 2:
+        events = [None] * steps
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -133,7 +137,7 @@ def timed_steps(step, n_events: int, steps: int, warmup: int):
         step(events[i])
     t1.record()
     torch.cuda.synchronize()
-    per = [0.0] * (n_events - 1)
+    per = [0.0] * max(n_events - 1, 0)
     for ev in events:
         for j in range(n_events - 1):
             per[j] += ev[j].elapsed_time(ev[j + 1])
@@ -217,6 +221,13 @@ def main():
     ws = torch.empty(max(ws_bytes, 256) // 4 + 64, device=dev) if ws_bytes else None
 
     def step(ev=None):
+        # the path as a caller runs it: one forward call, one backward call
+        mt.linear_fwd(x, wt, bias, y)
+        mt.linear_bwd(x, wt, dy, dx, dw, db, workspace=ws)
+
+    def step_per_kernel(ev=None):
+        # the same kernels, the backward issued one output at a time so that
+        # events bracket each kernel
         if ev is not None:
             ev[0].record()
         mt.linear_fwd(x, wt, bias, y)
@@ -232,7 +243,8 @@ def main():
         if ev is not None:
             ev[4].record()
 
-    total_ms_step, per_list = timed_steps(step, 5, args.steps, args.warmup)
+    total_ms_step, _ = timed_steps(step, 1, args.steps, args.warmup)
+    _, per_list = timed_steps(step_per_kernel, 5, args.steps, 1)
     per = dict(zip(["fwd_nt_gemm", "dx_nn_gemm", "dw_tn_gemm", "db_colsum"], per_list))
     total_ms = total_ms_step * args.steps
     ms_per_step = total_ms / args.steps

@@ -155,6 +155,18 @@ def test_reduce_validation():
     assert rd(G, D([6, 5], ptr=0x20000, stride=[1, 6])) == 5
 
 
+def test_pitch_beyond_tile_offset_range_rejected():
+    """Rows 2**25 floats apart: even the smallest tile (64 rows) would span
+    2**33 bytes of offsets, beyond the kernels' 32-bit range, so every tile
+    configuration rejects the call on the host with MT_ERR_LAYOUT."""
+    G = 1 << 40  # fake, well-separated addresses; nothing is dereferenced
+    x = b.raw_desc(G, F32, (300, 8), (1 << 25, 1))
+    w = b.raw_desc(2 * G, F32, (300, 8), (8, 1))
+    y = b.raw_desc(3 * G, F32, (300, 300), (300, 1))
+    assert fwd(x, w, None, y) == 5
+    assert "offset" in b.lib.mt_last_error().decode()
+
+
 def test_empty_problems_need_no_gpu():
     # M == 0 or N == 0: valid, nothing to do, nothing launched
     assert fwd(D([0, 4], ptr=0), D([6, 4], ptr=0x20000), None, D([0, 6], ptr=0)) == 0
