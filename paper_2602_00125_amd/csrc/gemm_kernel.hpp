@@ -84,9 +84,13 @@ template <int ESIZE, bool KC, int BMN, int BK, int VEC, int NT>
 struct Tile {
   // K-contiguous rows: +16 bytes (an odd multiple of 16 bytes between rows
   // keeps 16-byte reads of consecutive rows conflict-free). M/N-contiguous
-  // rows: fp32 +8 elements; bf16 +16 elements, so that the 4 rows read by a
-  // 16-lane group of ds_read_b64_tr_b16 start 32 bytes apart modulo 128.
-  static constexpr int PAD = KC ? 16 / ESIZE : (ESIZE == 2 ? 16 : 8);  // elements
+  // rows: fp32 +8 elements; bf16 +MT_BF16_MC_PAD elements (rows 64 bytes
+  // apart modulo 256: the 4 rows x 2 column halves that two 16-lane groups
+  // of ds_read_b64_tr_b16 read together fall on disjoint banks).
+#ifndef MT_BF16_MC_PAD
+#define MT_BF16_MC_PAD 32
+#endif
+  static constexpr int PAD = KC ? 16 / ESIZE : (ESIZE == 2 ? MT_BF16_MC_PAD : 8);  // elements
   static constexpr int PITCH = (KC ? BK : BMN) + PAD;       // elements per LDS row
   static constexpr int ROWS = KC ? BMN : BK;
   static constexpr int COLS = KC ? BK : BMN;                // contiguous extent
