@@ -164,7 +164,8 @@ mt_status mt_matmul_shape(int32_t na, const int64_t* a, int32_t nb, const int64_
 /* Testing and tuning knobs (process-wide, not thread-safe; 0 = accepted,
  * -1 = unknown key). Keys: "cfg" GEMM tile configuration (-1 = automatic,
  * 0 = 256x256, 1 = 256x128, 2 = 128x256, 3 = 128x128, 4 = 64x64,
- * 5 = 256x256 with 8 waves and BK = 64 for bf16, 256x256 for fp32);
+ * 5 = 256x256 with 8 waves (BK = 32 fp32, 64 bf16), 6 = 256x256 with 8 waves
+ * streaming tiles straight into a 4-stage LDS ring, 7 = the same with 4 waves);
  * "vec1" (1 = force the 4-byte-load kernels); "splits" (split-K count for
  * mt_linear_bwd's dw, 0 = automatic); "parts" (row slices of the db and
  * broadcast-gradient reductions, 0 = automatic). Results stay within the

@@ -92,16 +92,19 @@ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // work (measured faster than 256x256 on 8192^3). Smaller problems take
 // 128x128 when split-K can fill the chip, else 64x64.
 int choose_cfg(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_split, bool bf16,
-               bool both_kc) {
+               bool a_kc, bool b_kc) {
   if (g_force_cfg >= 0) return g_force_cfg;
   auto tiles = [&](int64_t bm, int64_t bn) { return cdiv(M, bm) * cdiv(N, bn) * batch; };
-  // bf16 moves half the bytes per flop of fp32 at 16x the matrix rate, so
-  // large bf16 products need the bigger 256x256 tile (twice the flops per
-  // loaded byte of 128x256) with 8 waves and BK = 64. For fp32 the 8-wave
-  // 256x256 tile (BK = 32) measured faster only when both operands are
-  // K-contiguous (Y = X W^T), whose 64-byte row segments per BK = 16 stage
-  // otherwise fetch half cache lines.
-  if (tiles(256, 256) >= 256 && (bf16 || both_kc)) return mt::kCfg256x256x64w8;
+  // Large products (measured on 8192^3 fp32 and 16384x8192x8192 bf16):
+  //  - bf16 moves half the bytes per flop of fp32 at 16x the matrix rate and
+  //    its K-stages are short, so it takes the 256x256 tile whose operands
+  //    stream straight into a 4-stage LDS ring (loads three stages ahead);
+  //  - fp32 takes the same kernel when A is K-contiguous (Y = X W^T and
+  //    dX = dY W); for dW = dY^T X (both operands M/N-contiguous) the
+  //    register-staged 128x256 / 256x128 tiles, two blocks per CU, measured
+  //    faster.
+  if (tiles(256, 256) >= 256 && (bf16 || a_kc)) return mt::kCfgDma256x256;
+  (void)b_kc;
   if (tiles(128, 256) >= 512) return N >= M ? mt::kCfg128x256 : mt::kCfg256x128;
   const int64_t t128 = tiles(128, 128);
   if (t128 >= 128) return mt::kCfg128x128;
@@ -159,7 +162,7 @@ size_t plan_gemm(GemmCall& g, bool may_split) {
   if (g_force_vec1) g.vec = false;
   const int64_t stages_guess = cdiv(p.K, g.bf16 ? 32 : 16) * p.red_count;
   if (g.cfg < 0)
-    g.cfg = choose_cfg(p.M, p.N, p.keep_count, stages_guess, may_split, g.bf16, g.a_kc && g.b_kc);
+    g.cfg = choose_cfg(p.M, p.N, p.keep_count, stages_guess, may_split, g.bf16, g.a_kc, g.b_kc);
   // the element-load kernels keep their staging registers within budget up to 128x128
   if (!g.vec && g.cfg != mt::kCfg64x64) g.cfg = mt::kCfg128x128;
   const int64_t stages = cdiv(p.K, mt::gemm_tile_k(g.cfg, g.bf16)) * p.red_count;

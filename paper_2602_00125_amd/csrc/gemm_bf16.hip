@@ -1,6 +1,7 @@
 // bf16 instantiations of the matrix-core GEMM (see gemm_kernel.hpp):
 // v_mfma_f32_32x32x16_bf16 (exact bf16 products, fp32 accumulation), BK = 32,
 // 16-byte (VEC = 8) or 2-byte (VEC = 1) loads; fp32 bias and output.
+#include "gemm_dma.hpp"
 #include "gemm_kernel.hpp"
 #include "kernels.hpp"
 
@@ -19,6 +20,19 @@ static hipError_t launch_bf16(const GemmParams& p, hipStream_t stream) {
   return hipGetLastError();
 }
 
+template <bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int WGN, int NS, int WPE>
+static hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
+  GemmParams q = p;
+  q.tiles_m = (int32_t)((p.M + BM - 1) / BM);
+  q.tiles_n = (int32_t)((p.N + BN - 1) / BN);
+  const int64_t blocks = (int64_t)q.tiles_m * q.tiles_n * p.keep_count * p.splits;
+  if (blocks <= 0) return hipSuccess;
+  if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL((gemm::gemm_dma_kernel<__bf16, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, WPE>),
+                     dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
+  return hipGetLastError();
+}
+
 template <bool A_KC, bool B_KC, int VEC>
 static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream) {
   if constexpr (VEC == 1) {
@@ -29,6 +43,8 @@ static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream
     switch (cfg) {
       case kCfg256x256: return launch_bf16<A_KC, B_KC, 256, 256, 32, 2, 2, VEC, 1>(p, stream);
       case kCfg256x256x64w8: return launch_bf16<A_KC, B_KC, 256, 256, 64, 2, 4, VEC, 2>(p, stream);
+      case kCfgDma256x256: return launch_dma<A_KC, B_KC, 256, 256, 32, 2, 4, 4, 2>(p, stream);
+      case kCfgDma256x256w4: return launch_dma<A_KC, B_KC, 256, 256, 32, 2, 2, 4, 1>(p, stream);
       case kCfg256x128: return launch_bf16<A_KC, B_KC, 256, 128, 32, 2, 2, VEC, 2>(p, stream);
       case kCfg128x256: return launch_bf16<A_KC, B_KC, 128, 256, 32, 2, 2, VEC, 2>(p, stream);
       case kCfg128x128: return launch_bf16<A_KC, B_KC, 128, 128, 32, 2, 2, VEC, 2>(p, stream);

@@ -1,0 +1,379 @@
+// Matrix-core GEMM whose operand tiles travel from HBM straight into LDS
+// (buffer_load_dwordx4 ... lds), gfx950 only. Same contract and epilogue as
+// gemm_kernel.hpp (MiniTensor Sec. 3.1 Eq. (1), Sec. 3.2 Eq. (4), Sec. 3.3
+// Eq. (5)); used for 16-byte-aligned operands of large products.
+//
+// Why: a bf16 K-stage is short (a 256x256x32 stage is ~0.4 us of matrix-core
+// work), shorter than an HBM round trip. With register staging only one
+// stage of loads can be in flight. Here the loads write LDS themselves, so
+// NS stages live in an LDS ring and loads run NS-1 stages ahead; no staging
+// registers, no ds_write instructions.
+//
+// LDS layout: each operand tile is stored without padding, in rows of
+// 16-byte chunks. The chunk index is XOR-swizzled with a function of the row
+// so that fragment reads hit distinct banks:
+//   K-contiguous tile, 64-byte rows:  chunk ^ (((r >> 1) & 3) ^ ((r >> 3) & 1))
+//   K-contiguous tile, 128-byte rows: chunk ^ ((r & 7) ^ ((r >> 3) & 1))
+//     (16 consecutive rows read at one chunk land on 16 distinct 16-byte bank
+//     slots of a 256-byte window, and 8 consecutive rows on 8 slots of 128 B)
+//   M/N-contiguous bf16 tile (rows of >= 256 bytes): chunk ^ (4 * (r & 3))
+//     (the 4 rows x 4 chunks that two 16-lane groups of ds_read_b64_tr_b16
+//     read together land on 16 distinct slots)
+//   M/N-contiguous fp32 tile: chunk ^ (8 * ((r >> 2) & 1)) (the two rows a
+//     4-byte read takes at once, k and k+4, fall in opposite 128-byte halves)
+// A DMA instruction writes 64 lanes x 16 bytes to 1 KB of consecutive LDS
+// (lane i at base + 16 i); each lane therefore loads the global chunk that
+// the swizzle places at its LDS slot.
+//
+// Pipeline per stage s: wait until this wave's loads of stage s have
+// landed (s_waitcnt vmcnt with the number of younger stages in flight),
+// barrier (every wave's loads landed; every wave finished stage s-1), issue
+// the loads of stage s+NS-1 into the slot stage s-1 used, then the MFMAs of
+// stage s. The barrier is a bare s_barrier: a release fence would make
+// every wave wait for all loads in flight, younger stages included.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include "gemm_kernel.hpp"
+#include "gemm_params.hpp"
+
+namespace mt {
+namespace gemm {
+
+// One 16-byte-per-lane load from a buffer straight into LDS: lane i's bytes
+// land at lds_byte + 16 i. Issued as assembly so that the compiler's wait
+// insertion, which cannot tell the LDS bytes these loads write from the ones
+// the MFMA fragments read, does not wait for every load in flight before
+// each LDS read; the kernel waits for exactly the stage it reads instead.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds_byte) {
+  __asm__ __volatile__("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                       :
+                       : "s"(lds_byte), "v"(voff), "s"(r)
+                       : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_byte_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+
+// s_waitcnt with only vmcnt limited (expcnt and lgkmcnt at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <int ES, bool KC, int BMN, int BK>
+struct DmaTile {
+  static constexpr int RB = KC ? BK * ES : BMN * ES;  // bytes per LDS row
+  static constexpr int ROWS = KC ? BMN : BK;
+  static constexpr int BYTES = ROWS * RB;
+  static constexpr int BLOCKS = BYTES / 1024;          // 1 KB DMA blocks per stage
+  static constexpr int EPC = 16 / ES;                   // elements per 16-byte chunk
+  static_assert(BYTES % 1024 == 0, "tile must be whole 1 KB blocks");
+  static_assert(!KC || RB == 64 || RB == 128, "K-contiguous rows of 64 or 128 bytes");
+  static_assert(KC || RB >= 256, "M/N-contiguous rows of at least 256 bytes");
+
+  static __device__ __forceinline__ int swz(int r) {
+    if constexpr (KC) {
+      if constexpr (RB == 64) return ((r >> 1) & 3) ^ ((r >> 3) & 1);
+      else return (r & 7) ^ ((r >> 3) & 1);
+    } else if constexpr (ES == 2) {
+      return 4 * (r & 3);
+    } else {
+      // fp32 4-byte reads: lanes 0-31 read row k, lanes 32-63 row k+4, the
+      // same 32 columns; rows k and k+4 go to opposite 128-byte halves
+      return 8 * ((r >> 2) & 1);
+    }
+  }
+  // byte address in the tile of element (row r, contiguous index c)
+  static __device__ __forceinline__ int addr(int r, int c) {
+    return r * RB + (((c / EPC) ^ swz(r)) * 16) + (c % EPC) * ES;
+  }
+};
+
+// Per-lane DMA plan of one operand: the wave issues JB instructions per stage.
+template <int ES, bool KC, int BMN, int BK, int NW>
+struct DmaLoader {
+  using T = DmaTile<ES, KC, BMN, BK>;
+  static constexpr int JB = T::BLOCKS / NW;
+  static_assert(T::BLOCKS % NW == 0, "blocks split evenly over the waves");
+  uint32_t off[JB];  // byte offset from the stage's tile origin in global memory
+  int row[JB], col[JB];
+
+  __device__ __forceinline__ void init(int wave, int lane, int64_t ld) {
+#pragma unroll
+    for (int j = 0; j < JB; ++j) {
+      const int b = wave + NW * j;
+      const int byte = 1024 * b + 16 * lane;
+      const int r = byte / T::RB;
+      const int pchunk = (byte % T::RB) / 16;
+      const int c = (pchunk ^ T::swz(r)) * T::EPC;
+      row[j] = r;
+      col[j] = c;
+      off[j] = (uint32_t)(((int64_t)r * ld + c) * ES);
+    }
+  }
+  // base: global element (row 0, col 0) of this stage's tile; lds: the tile's
+  // LDS origin. Out-of-range rows / columns read as zero.
+  __device__ __forceinline__ void issue(const char* base, int64_t rows_left, int64_t cols_left,
+                                        char* lds, int wave) const {
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(base);
+    const int rl = rows_left < T::ROWS ? (int)rows_left : T::ROWS;
+    const int cl = cols_left < (T::RB / ES) ? (int)cols_left : (T::RB / ES);
+    const uint32_t lds0 = lds_byte_addr(lds);
+#pragma unroll
+    for (int j = 0; j < JB; ++j) {
+      const bool ok = row[j] < rl && col[j] < cl;
+      dma16(r, ok ? off[j] : kOOB, lds0 + 1024 * (wave + NW * j));
+    }
+  }
+};
+
+template <typename T, bool A_KC, bool B_KC, int TM, int TN, int BK>
+struct DmaMma;
+
+// fp32: within a group of 8 k, step j (0..3) takes k = 8g + 4h + j for lane
+// half h (one 16-byte read of a K-contiguous tile feeds 4 steps).
+template <bool A_KC, bool B_KC, int TM, int TN, int BK>
+struct DmaMma<float, A_KC, B_KC, TM, TN, BK> {
+  template <bool KC, int BMN, int N>
+  static __device__ __forceinline__ void frag(const char* S, int mn0, int g, int lane,
+                                              float (&f)[4][N], int i) {
+    using Tl = DmaTile<4, KC, BMN, BK>;
+    const int h = lane >> 5, mn = mn0 + (lane & 31);
+    if constexpr (KC) {
+      const f32x4 v = *(const f32x4*)(S + Tl::addr(mn, 8 * g + 4 * h));
+      f[0][i] = v[0];
+      f[1][i] = v[1];
+      f[2][i] = v[2];
+      f[3][i] = v[3];
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) f[j][i] = *(const float*)(S + Tl::addr(8 * g + 4 * h + j, mn));
+    }
+  }
+  template <int BM, int BN>
+  static __device__ __forceinline__ void run(const char* As, const char* Bs, int am, int bn,
+                                             int lane, f32x16 (&acc)[TM][TN]) {
+#pragma unroll
+    for (int g = 0; g < BK / 8; ++g) {
+      float af[4][TM], bf[4][TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) frag<A_KC, BM, TM>(As, am + i * 32, g, lane, af, i);
+#pragma unroll
+      for (int i = 0; i < TN; ++i) frag<B_KC, BN, TN>(Bs, bn + i * 32, g, lane, bf, i);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int q = 0; q < TN; ++q)
+            acc[i][q] = __builtin_amdgcn_mfma_f32_32x32x2f32(bf[j][q], af[j][i], acc[i][q], 0, 0, 0);
+    }
+  }
+};
+
+// bf16: one MFMA step covers 16 k; lane half h supplies k = 16s + 8h + 0..7.
+template <bool A_KC, bool B_KC, int TM, int TN, int BK>
+struct DmaMma<__bf16, A_KC, B_KC, TM, TN, BK> {
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  template <bool KC, int BMN>
+  static __device__ __forceinline__ u16x8 frag(const char* S, int mn0, int k0, int lane) {
+    using Tl = DmaTile<2, KC, BMN, BK>;
+    if constexpr (KC) {
+      const int mn = mn0 + (lane & 31);
+      return *(const u16x8*)(S + Tl::addr(mn, k0));
+    } else {
+      // ds_read_b64_tr_b16: lane s of each 16-lane group addresses row
+      // k0 + s/4, columns c0 + 4 (s % 4); lane i then receives column c0 + i
+      // at rows k0 .. k0+3 (second read: rows k0+4 .. k0+7)
+      const int g = lane >> 4, s = lane & 15;
+      const int col = mn0 + 16 * (g & 1) + 4 * (s & 3);
+      const int r = k0 + (s >> 2);
+      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (lds_s16x4*)(const void*)(S + Tl::addr(r, col)));
+      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (lds_s16x4*)(const void*)(S + Tl::addr(r + 4, col)));
+      u16x8 v;
+      v[0] = lo[0]; v[1] = lo[1]; v[2] = lo[2]; v[3] = lo[3];
+      v[4] = hi[0]; v[5] = hi[1]; v[6] = hi[2]; v[7] = hi[3];
+      return v;
+    }
+  }
+  template <int BM, int BN>
+  static __device__ __forceinline__ void run(const char* As, const char* Bs, int am, int bn,
+                                             int lane, f32x16 (&acc)[TM][TN]) {
+    const int h = lane >> 5;
+#pragma unroll
+    for (int s = 0; s < BK / 16; ++s) {
+      const int k0 = 16 * s + 8 * h;
+      u16x8 af[TM], bf[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[i] = frag<A_KC, BM>(As, am + i * 32, k0, lane);
+#pragma unroll
+      for (int i = 0; i < TN; ++i) bf[i] = frag<B_KC, BN>(Bs, bn + i * 32, k0, lane);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int q = 0; q < TN; ++q)
+          acc[i][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, bf[q]),
+                                                               __builtin_bit_cast(bf16x8, af[i]),
+                                                               acc[i][q], 0, 0, 0);
+    }
+  }
+};
+
+template <typename T, bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int WGN, int NS,
+          int WAVES_PER_EU>
+__global__ __launch_bounds__(WGM * WGN * 64)
+__attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
+void gemm_dma_kernel(const GemmParams p) {
+  constexpr int ES = (int)sizeof(T);
+  constexpr int NW = WGM * WGN;
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  static_assert(NS == 3 || NS == 4, "three or four stages in the ring");
+  using LA = DmaLoader<ES, A_KC, BM, BK, NW>;
+  using LB = DmaLoader<ES, B_KC, BN, BK, NW>;
+  constexpr int A_BYTES = LA::T::BYTES, B_BYTES = LB::T::BYTES;
+  constexpr int STAGE = A_BYTES + B_BYTES;
+  constexpr int L = LA::JB + LB::JB;  // DMA instructions per wave per stage
+  __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (LDS DMA base)
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int l32 = lane & 31, h = lane >> 5;
+
+  // ---- block -> (split, batch, tile), as in gemm_kernel
+  const int64_t tiles = (int64_t)p.tiles_m * p.tiles_n;
+  int64_t logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t t = logical % tiles;
+  logical /= tiles;
+  const int64_t batch = logical % p.keep_count;
+  const int split = (int)(logical / p.keep_count);
+  int tm_idx, tn_idx;
+  {
+    const int64_t width = (int64_t)p.group_m * p.tiles_n;
+    const int64_t gid = t / width;
+    const int64_t first = gid * p.group_m;
+    const int64_t gsz = (p.tiles_m - first) < p.group_m ? (p.tiles_m - first) : p.group_m;
+    tm_idx = (int)(first + (t % width) % gsz);
+    tn_idx = (int)((t % width) / gsz);
+  }
+  const int64_t m0 = (int64_t)tm_idx * BM, n0 = (int64_t)tn_idx * BN;
+  int64_t a_off = 0, b_off = 0, c_off = 0;
+  {
+    int64_t rem = batch;
+    for (int d = p.nkeep - 1; d >= 0; --d) {
+      const int64_t i = rem % p.keep_shape[d];
+      rem /= p.keep_shape[d];
+      a_off += i * p.keep_sa[d];
+      b_off += i * p.keep_sb[d];
+      c_off += i * p.keep_sc[d];
+    }
+  }
+  const char* A = (const char*)p.a + a_off * ES;
+  const char* B = (const char*)p.b + b_off * ES;
+
+  const int64_t KS = (p.K + BK - 1) / BK;
+  const int64_t S_all = KS * p.red_count;
+  const int64_t st0 = (int64_t)split * p.stages_per_split;
+  const int64_t st1 = (st0 + p.stages_per_split) < S_all ? (st0 + p.stages_per_split) : S_all;
+  const int S = st1 > st0 ? (int)(st1 - st0) : 0;
+
+  LA la;
+  LB lb;
+  la.init(wave, lane, p.lda);
+  lb.init(wave, lane, p.ldb);
+
+  // issue cursor: (summed batch index r, k tile kt) of the next stage to load
+  int64_t cur_r = KS > 0 ? st0 / KS : 0, cur_kt = KS > 0 ? st0 % KS : 0;
+  int64_t ra_off = 0, rb_off = 0;
+  auto red_offsets = [&](int64_t r) {
+    ra_off = 0;
+    rb_off = 0;
+    for (int d = p.nred - 1; d >= 0; --d) {
+      const int64_t i = r % p.red_shape[d];
+      r /= p.red_shape[d];
+      ra_off += i * p.red_sa[d];
+      rb_off += i * p.red_sb[d];
+    }
+  };
+  if (S > 0 && p.nred > 0) red_offsets(cur_r);
+  auto issue_next = [&](int slot) {
+    const int64_t k0 = cur_kt * BK;
+    const char* Ar = A + ra_off * ES;
+    const char* Br = B + rb_off * ES;
+    char* dst = lds + slot * STAGE;
+    if (A_KC) la.issue(Ar + (m0 * p.lda + k0) * ES, p.M - m0, p.K - k0, dst, wave);
+    else la.issue(Ar + (k0 * p.lda + m0) * ES, p.K - k0, p.M - m0, dst, wave);
+    if (B_KC) lb.issue(Br + (n0 * p.ldb + k0) * ES, p.N - n0, p.K - k0, dst + A_BYTES, wave);
+    else lb.issue(Br + (k0 * p.ldb + n0) * ES, p.K - k0, p.N - n0, dst + A_BYTES, wave);
+    if (++cur_kt == KS) {
+      cur_kt = 0;
+      ++cur_r;
+      if (cur_r < p.red_count) red_offsets(cur_r);
+    }
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
+
+  // prologue: stages 0 .. NS-2 in flight
+#pragma unroll
+  for (int q = 0; q < NS - 1; ++q)
+    if (q < S) issue_next(q);
+
+  for (int s = 0; s < S; ++s) {
+    // this wave's loads of stage s have landed once at most `ahead` younger
+    // stages (of L instructions each) are still in flight
+    const int ahead = (S - 1 - s) < (NS - 2) ? (S - 1 - s) : (NS - 2);
+    if (ahead == 2) wait_vmcnt<2 * L>();
+    else if (ahead == 1) wait_vmcnt<L>();
+    else wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    __asm__ __volatile__("" ::: "memory");
+    if (s + NS - 1 < S) issue_next((s + NS - 1) % NS);
+    const char* st = lds + (s % NS) * STAGE;
+    DmaMma<T, A_KC, B_KC, TM, TN, BK>::template run<BM, BN>(st, st + A_BYTES, wm * WTM, wn * WTN,
+                                                            lane, acc);
+    __asm__ __volatile__("" ::: "memory");
+  }
+
+  // ---- epilogue (as in gemm_kernel): lane holds C[m][n0' + 8g + 4h + 0..3]
+  const bool to_partial = p.splits > 1;
+  float* C = to_partial ? p.partial + (int64_t)split * p.partial_stride + batch * p.M * p.N
+                        : p.c + c_off;
+  const int64_t ldc = to_partial ? p.N : p.ldc;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int64_t m = m0 + wm * WTM + i * 32 + l32;
+    if (m >= p.M) continue;
+    float* crow = C + m * ldc;
+#pragma unroll
+    for (int q = 0; q < TN; ++q) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int64_t n = n0 + wn * WTN + q * 32 + 8 * g + 4 * h;
+        if (n >= p.N) continue;
+        f32x4 v = {acc[i][q][4 * g + 0], acc[i][q][4 * g + 1], acc[i][q][4 * g + 2],
+                   acc[i][q][4 * g + 3]};
+        if (!to_partial) {
+          if (p.bias) v += *(const f32x4*)&p.bias[n];
+          if (p.accumulate) v += *(const f32x4*)&crow[n];
+        }
+        *(f32x4*)&crow[n] = v;
+      }
+    }
+  }
+}
+
+}  // namespace gemm
+}  // namespace mt

@@ -1,5 +1,6 @@
 // fp32 instantiations of the matrix-core GEMM (see gemm_kernel.hpp):
 // v_mfma_f32_32x32x2_f32, BK = 16, 16-byte (VEC = 4) or 4-byte (VEC = 1) loads.
+#include "gemm_dma.hpp"
 #include "gemm_kernel.hpp"
 #include "kernels.hpp"
 
@@ -18,6 +19,19 @@ static hipError_t launch_f32(const GemmParams& p, hipStream_t stream) {
   return hipGetLastError();
 }
 
+template <bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int WGN, int NS, int WPE>
+static hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
+  GemmParams q = p;
+  q.tiles_m = (int32_t)((p.M + BM - 1) / BM);
+  q.tiles_n = (int32_t)((p.N + BN - 1) / BN);
+  const int64_t blocks = (int64_t)q.tiles_m * q.tiles_n * p.keep_count * p.splits;
+  if (blocks <= 0) return hipSuccess;
+  if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL((gemm::gemm_dma_kernel<float, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, WPE>),
+                     dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
+  return hipGetLastError();
+}
+
 template <bool A_KC, bool B_KC, int VEC>
 static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream) {
   if constexpr (VEC == 1) {
@@ -26,6 +40,8 @@ static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream
     return launch_f32<A_KC, B_KC, 128, 128, 16, 2, 2, 1, 2>(p, stream);
   } else {
     switch (cfg) {
+      case kCfgDma256x256: return launch_dma<A_KC, B_KC, 256, 256, 16, 2, 4, 4, 2>(p, stream);
+      case kCfgDma256x256w4: return launch_dma<A_KC, B_KC, 256, 256, 16, 2, 2, 4, 1>(p, stream);
       case kCfg256x256: return launch_f32<A_KC, B_KC, 256, 256, 16, 2, 2, VEC, 1>(p, stream);
       case kCfg256x256x64w8: return launch_f32<A_KC, B_KC, 256, 256, 32, 2, 4, VEC, 2>(p, stream);
       case kCfg256x128: return launch_f32<A_KC, B_KC, 256, 128, 16, 2, 2, VEC, 2>(p, stream);
@@ -38,20 +54,23 @@ static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream
 
 int gemm_tile_m(int cfg) {
   switch (cfg) {
-    case kCfg256x256: case kCfg256x128: case kCfg256x256x64w8: return 256;
+    case kCfg256x256: case kCfg256x128: case kCfg256x256x64w8: case kCfgDma256x256:
+    case kCfgDma256x256w4: return 256;
     case kCfg128x256: case kCfg128x128: return 128;
     default: return 64;
   }
 }
 int gemm_tile_n(int cfg) {
   switch (cfg) {
-    case kCfg256x256: case kCfg128x256: case kCfg256x256x64w8: return 256;
+    case kCfg256x256: case kCfg128x256: case kCfg256x256x64w8: case kCfgDma256x256:
+    case kCfgDma256x256w4: return 256;
     case kCfg256x128: case kCfg128x128: return 128;
     default: return 64;
   }
 }
 int gemm_tile_k(int cfg, bool bf16) {
   if (cfg == kCfg256x256x64w8) return bf16 ? 64 : 32;
+  if (cfg == kCfgDma256x256 || cfg == kCfgDma256x256w4) return bf16 ? 32 : 16;
   return bf16 ? 32 : 16;
 }
 

@@ -17,7 +17,9 @@ enum GemmCfg {
   kCfg128x256 = 2,
   kCfg128x128 = 3,
   kCfg64x64 = 4,
-  kCfg256x256x64w8 = 5
+  kCfg256x256x64w8 = 5,
+  kCfgDma256x256 = 6,   // 256x256, 8 waves, tiles loaded straight into a 4-stage LDS ring
+  kCfgDma256x256w4 = 7  // the same with 4 waves (128x128 per wave)
 };
 int gemm_tile_m(int cfg);
 int gemm_tile_n(int cfg);
