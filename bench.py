@@ -33,9 +33,11 @@ METRIC = "TFLOP/s for linear fwd+bwd (3 GEMMs) at M=N=K=8192 fp32; % MFMA peak"
 # sources whose text decides each measured kernel (counters taken on other
 # sources are stale and not reported)
 KERNEL_SOURCES = {
-    "gemm": ["paper_2602_00125_amd/csrc/gemm_kernel.hpp", "paper_2602_00125_amd/csrc/gemm_f32.hip",
+    "gemm": ["paper_2602_00125_amd/csrc/gemm_kernel.hpp", "paper_2602_00125_amd/csrc/gemm_dma.hpp",
+             "paper_2602_00125_amd/csrc/gemm_f32.hip",
              "paper_2602_00125_amd/csrc/gemm_params.hpp", "paper_2602_00125_amd/csrc/capi.cpp"],
-    "gemm_bf16": ["paper_2602_00125_amd/csrc/gemm_kernel.hpp", "paper_2602_00125_amd/csrc/gemm_bf16.hip",
+    "gemm_bf16": ["paper_2602_00125_amd/csrc/gemm_kernel.hpp", "paper_2602_00125_amd/csrc/gemm_dma.hpp",
+                  "paper_2602_00125_amd/csrc/gemm_bf16.hip",
                   "paper_2602_00125_amd/csrc/gemm_params.hpp", "paper_2602_00125_amd/csrc/capi.cpp"],
     "colsum": ["paper_2602_00125_amd/csrc/reduce.hip", "paper_2602_00125_amd/csrc/capi.cpp"],
 }

@@ -95,16 +95,14 @@ int choose_cfg(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_spl
                bool a_kc, bool b_kc) {
   if (g_force_cfg >= 0) return g_force_cfg;
   auto tiles = [&](int64_t bm, int64_t bn) { return cdiv(M, bm) * cdiv(N, bn) * batch; };
-  // Large products (measured on 8192^3 fp32 and 16384x8192x8192 bf16):
-  //  - bf16 moves half the bytes per flop of fp32 at 16x the matrix rate and
-  //    its K-stages are short, so it takes the 256x256 tile whose operands
-  //    stream straight into a 4-stage LDS ring (loads three stages ahead);
-  //  - fp32 takes the same kernel when A is K-contiguous (Y = X W^T and
-  //    dX = dY W); for dW = dY^T X (both operands M/N-contiguous) the
-  //    register-staged 128x256 / 256x128 tiles, two blocks per CU, measured
-  //    faster.
-  if (tiles(256, 256) >= 256 && (bf16 || a_kc)) return mt::kCfgDma256x256;
+  // Large products (measured on 8192^3 fp32 and 16384x8192x8192 bf16, all
+  // three layouts): the 256x256 tile whose operands stream straight into a
+  // two-stage LDS ring, one block of 8 waves per CU, once there are enough
+  // tiles to fill every CU.
+  if (tiles(256, 256) >= 256) return mt::kCfgDma256x256;
+  (void)a_kc;
   (void)b_kc;
+  (void)bf16;
   if (tiles(128, 256) >= 512) return N >= M ? mt::kCfg128x256 : mt::kCfg256x128;
   const int64_t t128 = tiles(128, 128);
   if (t128 >= 128) return mt::kCfg128x128;

@@ -3,11 +3,14 @@
 // gemm_kernel.hpp (MiniTensor Sec. 3.1 Eq. (1), Sec. 3.2 Eq. (4), Sec. 3.3
 // Eq. (5)); used for 16-byte-aligned operands of large products.
 //
-// Why: a bf16 K-stage is short (a 256x256x32 stage is ~0.4 us of matrix-core
-// work), shorter than an HBM round trip. With register staging only one
-// stage of loads can be in flight. Here the loads write LDS themselves, so
-// NS stages live in an LDS ring and loads run NS-1 stages ahead; no staging
-// registers, no ds_write instructions.
+// Why: the loads write LDS themselves, so no staging registers and no
+// ds_write instructions sit between HBM and the fragments. Tiles are
+// 256x256 with BK = 32 (fp32) or 64 (bf16), i.e. 64 KB per stage, and the
+// ring holds NS = 2 stages (128 KB of the 160 KB LDS): one stage is ~3 us of
+// fp32 or ~1 us of bf16 matrix work at 256x256, long enough for its
+// successor's loads to land, and the per-stage costs (barrier, first
+// fragment reads, load issue) are paid half as often as with BK = 16 / 32
+// in a deeper ring. The kernel accepts rings of 2 to 5 stages.
 //
 // LDS layout: each operand tile is stored without padding, in rows of
 // 16-byte chunks. The chunk index is XOR-swizzled with a function of the row
@@ -25,12 +28,15 @@
 // (lane i at base + 16 i); each lane therefore loads the global chunk that
 // the swizzle places at its LDS slot.
 //
-// Pipeline per stage s: wait until this wave's loads of stage s have
-// landed (s_waitcnt vmcnt with the number of younger stages in flight),
-// barrier (every wave's loads landed; every wave finished stage s-1), issue
-// the loads of stage s+NS-1 into the slot stage s-1 used, then the MFMAs of
-// stage s. The barrier is a bare s_barrier: a release fence would make
-// every wave wait for all loads in flight, younger stages included.
+// Pipeline per stage s: wait until this wave's loads of stage s have landed
+// (s_waitcnt vmcnt with the number of younger stages in flight), barrier
+// (every wave's loads of stage s landed; every wave finished reading stage
+// s-1), then the k-steps of stage s, each k-step's fragments read from LDS
+// while the previous k-step's MFMAs run. The loads of stage s+NS-1 (into
+// the slot of stage s-1) go out after the first k-step's MFMAs are issued,
+// so their address arithmetic overlaps matrix work. The barrier is a bare
+// s_barrier: a release fence would make every wave wait for all loads in
+// flight, younger stages included.
 #pragma once
 #include <hip/hip_runtime.h>
 
@@ -45,11 +51,23 @@ namespace gemm {
 // insertion, which cannot tell the LDS bytes these loads write from the ones
 // the MFMA fragments read, does not wait for every load in flight before
 // each LDS read; the kernel waits for exactly the stage it reads instead.
+// An LDS-DMA load that reads M0 right after a scalar write of M0 needs one
+// wait state in between (the s_nop).
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds_byte) {
-  __asm__ __volatile__("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+  __asm__ __volatile__("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                        :
                        : "s"(lds_byte), "v"(voff), "s"(r)
                        : "memory", "m0");
+}
+
+// The same address in every lane, taken from lane 0: the compiler may keep a
+// wave-uniform 64-bit offset in vector registers (after a 64-bit division),
+// and the LDS-DMA load takes its buffer descriptor in scalar registers only.
+__device__ __forceinline__ const char* uniform_ptr(const char* p) {
+  const uint64_t v = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (const char*)(uintptr_t)(((uint64_t)hi << 32) | lo);
 }
 
 __device__ __forceinline__ uint32_t lds_byte_addr(const void* p) {
@@ -118,7 +136,7 @@ struct DmaLoader {
   // LDS origin. Out-of-range rows / columns read as zero.
   __device__ __forceinline__ void issue(const char* base, int64_t rows_left, int64_t cols_left,
                                         char* lds, int wave) const {
-    const __amdgpu_buffer_rsrc_t r = make_rsrc(base);
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(uniform_ptr(base));
     const int rl = rows_left < T::ROWS ? (int)rows_left : T::ROWS;
     const int cl = cols_left < (T::RB / ES) ? (int)cols_left : (T::RB / ES);
     const uint32_t lds0 = lds_byte_addr(lds);
@@ -130,13 +148,20 @@ struct DmaLoader {
   }
 };
 
-template <typename T, bool A_KC, bool B_KC, int TM, int TN, int BK>
+// Fragment loads and MFMAs of one k-step, split so that the next k-step's
+// fragments (across stages, too) load while the current k-step multiplies.
+template <typename T, bool A_KC, bool B_KC, int TM, int TN, int BK, int BM, int BN>
 struct DmaMma;
 
-// fp32: within a group of 8 k, step j (0..3) takes k = 8g + 4h + j for lane
-// half h (one 16-byte read of a K-contiguous tile feeds 4 steps).
-template <bool A_KC, bool B_KC, int TM, int TN, int BK>
-struct DmaMma<float, A_KC, B_KC, TM, TN, BK> {
+// fp32: a k-step is a group of 8 k; within it, MFMA step j (0..3) takes
+// k = 8g + 4h + j for lane half h (one 16-byte read of a K-contiguous tile
+// feeds 4 steps).
+template <bool A_KC, bool B_KC, int TM, int TN, int BK, int BM, int BN>
+struct DmaMma<float, A_KC, B_KC, TM, TN, BK, BM, BN> {
+  static constexpr int KSTEPS = BK / 8;
+  struct Frags {
+    float a[4][TM], b[4][TN];
+  };
   template <bool KC, int BMN, int N>
   static __device__ __forceinline__ void frag(const char* S, int mn0, int g, int lane,
                                               float (&f)[4][N], int i) {
@@ -153,30 +178,31 @@ struct DmaMma<float, A_KC, B_KC, TM, TN, BK> {
       for (int j = 0; j < 4; ++j) f[j][i] = *(const float*)(S + Tl::addr(8 * g + 4 * h + j, mn));
     }
   }
-  template <int BM, int BN>
-  static __device__ __forceinline__ void run(const char* As, const char* Bs, int am, int bn,
-                                             int lane, f32x16 (&acc)[TM][TN]) {
+  static __device__ __forceinline__ void load(const char* As, const char* Bs, int am, int bn,
+                                              int lane, int g, Frags& f) {
 #pragma unroll
-    for (int g = 0; g < BK / 8; ++g) {
-      float af[4][TM], bf[4][TN];
+    for (int i = 0; i < TM; ++i) frag<A_KC, BM, TM>(As, am + i * 32, g, lane, f.a, i);
 #pragma unroll
-      for (int i = 0; i < TM; ++i) frag<A_KC, BM, TM>(As, am + i * 32, g, lane, af, i);
+    for (int i = 0; i < TN; ++i) frag<B_KC, BN, TN>(Bs, bn + i * 32, g, lane, f.b, i);
+  }
+  static __device__ __forceinline__ void compute(const Frags& f, f32x16 (&acc)[TM][TN]) {
 #pragma unroll
-      for (int i = 0; i < TN; ++i) frag<B_KC, BN, TN>(Bs, bn + i * 32, g, lane, bf, i);
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int q = 0; q < TN; ++q)
-            acc[i][q] = __builtin_amdgcn_mfma_f32_32x32x2f32(bf[j][q], af[j][i], acc[i][q], 0, 0, 0);
-    }
+        for (int q = 0; q < TN; ++q)
+          acc[i][q] = __builtin_amdgcn_mfma_f32_32x32x2f32(f.b[j][q], f.a[j][i], acc[i][q], 0, 0, 0);
   }
 };
 
-// bf16: one MFMA step covers 16 k; lane half h supplies k = 16s + 8h + 0..7.
-template <bool A_KC, bool B_KC, int TM, int TN, int BK>
-struct DmaMma<__bf16, A_KC, B_KC, TM, TN, BK> {
+// bf16: a k-step covers 16 k; lane half h supplies k = 16s + 8h + 0..7.
+template <bool A_KC, bool B_KC, int TM, int TN, int BK, int BM, int BN>
+struct DmaMma<__bf16, A_KC, B_KC, TM, TN, BK, BM, BN> {
+  static constexpr int KSTEPS = BK / 16;
+  struct Frags {
+    u16x8 a[TM], b[TN];
+  };
   typedef short s16x4 __attribute__((ext_vector_type(4)));
   typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
   template <bool KC, int BMN>
@@ -202,30 +228,27 @@ struct DmaMma<__bf16, A_KC, B_KC, TM, TN, BK> {
       return v;
     }
   }
-  template <int BM, int BN>
-  static __device__ __forceinline__ void run(const char* As, const char* Bs, int am, int bn,
-                                             int lane, f32x16 (&acc)[TM][TN]) {
-    const int h = lane >> 5;
+  static __device__ __forceinline__ void load(const char* As, const char* Bs, int am, int bn,
+                                              int lane, int ks, Frags& f) {
+    const int k0 = 16 * ks + 8 * (lane >> 5);
 #pragma unroll
-    for (int s = 0; s < BK / 16; ++s) {
-      const int k0 = 16 * s + 8 * h;
-      u16x8 af[TM], bf[TN];
+    for (int i = 0; i < TM; ++i) f.a[i] = frag<A_KC, BM>(As, am + i * 32, k0, lane);
 #pragma unroll
-      for (int i = 0; i < TM; ++i) af[i] = frag<A_KC, BM>(As, am + i * 32, k0, lane);
+    for (int i = 0; i < TN; ++i) f.b[i] = frag<B_KC, BN>(Bs, bn + i * 32, k0, lane);
+  }
+  static __device__ __forceinline__ void compute(const Frags& f, f32x16 (&acc)[TM][TN]) {
 #pragma unroll
-      for (int i = 0; i < TN; ++i) bf[i] = frag<B_KC, BN>(Bs, bn + i * 32, k0, lane);
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int q = 0; q < TN; ++q)
-          acc[i][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, bf[q]),
-                                                               __builtin_bit_cast(bf16x8, af[i]),
-                                                               acc[i][q], 0, 0, 0);
-    }
+      for (int q = 0; q < TN; ++q)
+        acc[i][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, f.b[q]),
+                                                             __builtin_bit_cast(bf16x8, f.a[i]),
+                                                             acc[i][q], 0, 0, 0);
   }
 };
 
 template <typename T, bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int WGN, int NS,
+          int ISSUE_AT,
           int WAVES_PER_EU>
 __global__ __launch_bounds__(WGM * WGN * 64)
 __attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
@@ -234,7 +257,8 @@ void gemm_dma_kernel(const GemmParams p) {
   constexpr int NW = WGM * WGN;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
-  static_assert(NS == 3 || NS == 4, "three or four stages in the ring");
+  static_assert(NS >= 2 && NS <= 5, "a ring of two to five stages");
+  static_assert(ISSUE_AT >= 0 && ISSUE_AT < BK / (sizeof(T) == 4 ? 8 : 16), "issue point is a k-step");
   using LA = DmaLoader<ES, A_KC, BM, BK, NW>;
   using LB = DmaLoader<ES, B_KC, BN, BK, NW>;
   constexpr int A_BYTES = LA::T::BYTES, B_BYTES = LB::T::BYTES;
@@ -326,24 +350,40 @@ void gemm_dma_kernel(const GemmParams p) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
 
+  using Mma = DmaMma<T, A_KC, B_KC, TM, TN, BK, BM, BN>;
+  typename Mma::Frags cur, nxt;
+  const int am = wm * WTM, bn = wn * WTN;
+
   // prologue: stages 0 .. NS-2 in flight
 #pragma unroll
   for (int q = 0; q < NS - 1; ++q)
     if (q < S) issue_next(q);
 
   for (int s = 0; s < S; ++s) {
-    // this wave's loads of stage s have landed once at most `ahead` younger
-    // stages (of L instructions each) are still in flight
-    const int ahead = (S - 1 - s) < (NS - 2) ? (S - 1 - s) : (NS - 2);
-    if (ahead == 2) wait_vmcnt<2 * L>();
-    else if (ahead == 1) wait_vmcnt<L>();
-    else wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();
-    __asm__ __volatile__("" ::: "memory");
-    if (s + NS - 1 < S) issue_next((s + NS - 1) % NS);
+    // this wave's loads of stage s have landed once at most `younger` later
+    // stages (of L loads each) are still in flight; the barrier then makes
+    // every wave's loads visible and frees the slot stage s-1 used
+    {
+      const int issued = (s + NS - 2) < (S - 1) ? (s + NS - 2) : (S - 1);
+      const int younger = issued - s;
+      if (NS >= 5 && younger >= 3) wait_vmcnt<3 * L>();
+      else if (NS >= 4 && younger >= 2) wait_vmcnt<2 * L>();
+      else if (NS >= 3 && younger == 1) wait_vmcnt<L>();
+      else wait_vmcnt<0>();
+      __builtin_amdgcn_s_barrier();
+      __asm__ __volatile__("" ::: "memory");
+    }
     const char* st = lds + (s % NS) * STAGE;
-    DmaMma<T, A_KC, B_KC, TM, TN, BK>::template run<BM, BN>(st, st + A_BYTES, wm * WTM, wn * WTN,
-                                                            lane, acc);
+    Mma::load(st, st + A_BYTES, am, bn, lane, 0, cur);
+#pragma unroll
+    for (int ks = 0; ks < Mma::KSTEPS; ++ks) {
+      if (ks + 1 < Mma::KSTEPS) Mma::load(st, st + A_BYTES, am, bn, lane, ks + 1, nxt);
+      Mma::compute(cur, acc);
+      // the next stage's loads go out behind the first k-step's MFMAs, so
+      // that their address arithmetic and issue overlap matrix work
+      if (ks == ISSUE_AT && s + NS - 1 < S) issue_next((s + NS - 1) % NS);
+      cur = nxt;
+    }
     __asm__ __volatile__("" ::: "memory");
   }
 

@@ -27,7 +27,7 @@ static hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
   const int64_t blocks = (int64_t)q.tiles_m * q.tiles_n * p.keep_count * p.splits;
   if (blocks <= 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((gemm::gemm_dma_kernel<float, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, WPE>),
+  hipLaunchKernelGGL((gemm::gemm_dma_kernel<float, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 0, WPE>),
                      dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
   return hipGetLastError();
 }
@@ -40,8 +40,8 @@ static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream
     return launch_f32<A_KC, B_KC, 128, 128, 16, 2, 2, 1, 2>(p, stream);
   } else {
     switch (cfg) {
-      case kCfgDma256x256: return launch_dma<A_KC, B_KC, 256, 256, 16, 2, 4, 4, 2>(p, stream);
-      case kCfgDma256x256w4: return launch_dma<A_KC, B_KC, 256, 256, 16, 2, 2, 4, 1>(p, stream);
+      case kCfgDma256x256: return launch_dma<A_KC, B_KC, 256, 256, 32, 2, 4, 2, 2>(p, stream);
+      case kCfgDma256x256w4: return launch_dma<A_KC, B_KC, 256, 256, 32, 2, 2, 2, 1>(p, stream);
       case kCfg256x256: return launch_f32<A_KC, B_KC, 256, 256, 16, 2, 2, VEC, 1>(p, stream);
       case kCfg256x256x64w8: return launch_f32<A_KC, B_KC, 256, 256, 32, 2, 4, VEC, 2>(p, stream);
       case kCfg256x128: return launch_f32<A_KC, B_KC, 256, 128, 16, 2, 2, VEC, 2>(p, stream);
@@ -70,7 +70,7 @@ int gemm_tile_n(int cfg) {
 }
 int gemm_tile_k(int cfg, bool bf16) {
   if (cfg == kCfg256x256x64w8) return bf16 ? 64 : 32;
-  if (cfg == kCfgDma256x256 || cfg == kCfgDma256x256w4) return bf16 ? 32 : 16;
+  if (cfg == kCfgDma256x256 || cfg == kCfgDma256x256w4) return bf16 ? 64 : 32;
   return bf16 ? 32 : 16;
 }
 
