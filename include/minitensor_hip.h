@@ -162,13 +162,15 @@ mt_status mt_matmul_shape(int32_t na, const int64_t* a, int32_t nb, const int64_
                           int32_t* nout, int64_t* out);
 
 /* Testing and tuning knobs (process-wide, not thread-safe; 0 = accepted,
- * -1 = unknown key). Keys: "cfg" GEMM tile configuration (-1 = automatic,
- * 0 = 256x256, 1 = 256x128, 2 = 128x256, 3 = 128x128, 4 = 64x64,
- * 5 = 256x256 with 8 waves (BK = 32 fp32, 64 bf16), 6 = 256x256 with 8 waves
- * streaming tiles straight into a 4-stage LDS ring, 7 = the same with 4 waves);
- * "vec1" (1 = force the 4-byte-load kernels); "splits" (split-K count for
- * mt_linear_bwd's dw, 0 = automatic); "parts" (row slices of the db and
- * broadcast-gradient reductions, 0 = automatic). Results stay within the
+ * -1 = unknown key, -2 = value out of range). Keys: "cfg" GEMM tile
+ * configuration (-1 = automatic; register-staged tiles 0 = 256x256,
+ * 1 = 256x128, 2 = 128x256, 3 = 128x128, 4 = 64x64, 5 = 256x256 with 8 waves;
+ * tiles streamed straight into an LDS ring 6 = 256x256 with 8 waves,
+ * 7 = 256x256 with 4 waves, 8 = 256x128, 9 = 128x256; operands that do not
+ * allow 16-byte loads run at 128x128 or 64x64 whatever is forced); "vec1"
+ * (1 = force the narrow-load kernels); "splits" (0..4096, split-K count for
+ * mt_linear_bwd's dw, 0 = automatic); "parts" (0..4096, row slices of the db
+ * and broadcast-gradient reductions, 0 = automatic). Results stay within the
  * documented accuracy for every setting. */
 int mt_debug_set(const char* key, int64_t value);
 

@@ -196,8 +196,11 @@ def matmul_shape(a, b) -> tuple:
 
 
 def debug_set(key: str, value: int) -> None:
-    if lib.mt_debug_set(key.encode(), int(value)) != 0:
+    rc = lib.mt_debug_set(key.encode(), int(value))
+    if rc == -1:
         raise KeyError(key)
+    if rc != 0:
+        raise ValueError(f"{key}={value} out of range")
 
 
 def status_str(code: int) -> str:

@@ -649,11 +649,18 @@ const char* mt_last_error(void) { return g_err.c_str(); }
 
 int mt_debug_set(const char* key, int64_t value) {
   if (!key) return -1;
-  if (!std::strcmp(key, "cfg")) g_force_cfg = (int)value;
-  else if (!std::strcmp(key, "vec1")) g_force_vec1 = (int)value;
-  else if (!std::strcmp(key, "splits")) g_force_splits = (int)value;
-  else if (!std::strcmp(key, "parts")) g_force_parts = (int)value;
-  else return -1;
+  if (!std::strcmp(key, "cfg")) {
+    if (value < -1 || value >= mt::kNumGemmCfg) return -2;
+    g_force_cfg = (int)value;
+  } else if (!std::strcmp(key, "vec1")) {
+    if (value < 0 || value > 1) return -2;
+    g_force_vec1 = (int)value;
+  } else if (!std::strcmp(key, "splits") || !std::strcmp(key, "parts")) {
+    if (value < 0 || value > 4096) return -2;
+    (key[0] == 's' ? g_force_splits : g_force_parts) = (int)value;
+  } else {
+    return -1;
+  }
   return 0;
 }
 

@@ -28,7 +28,7 @@ static hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
   const int64_t blocks = (int64_t)q.tiles_m * q.tiles_n * p.keep_count * p.splits;
   if (blocks <= 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((gemm::gemm_dma_kernel<__bf16, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 0, WPE>),
+  hipLaunchKernelGGL((gemm::gemm_dma_kernel<__bf16, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 1, 1, WPE>),
                      dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
   return hipGetLastError();
 }
@@ -45,6 +45,8 @@ static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream
       case kCfg256x256x64w8: return launch_bf16<A_KC, B_KC, 256, 256, 64, 2, 4, VEC, 2>(p, stream);
       case kCfgDma256x256: return launch_dma<A_KC, B_KC, 256, 256, 64, 2, 4, 2, 2>(p, stream);
       case kCfgDma256x256w4: return launch_dma<A_KC, B_KC, 256, 256, 64, 2, 2, 2, 1>(p, stream);
+      case kCfgDma256x128: return launch_dma<A_KC, B_KC, 256, 128, 32, 2, 2, 3, 2>(p, stream);
+      case kCfgDma128x256: return launch_dma<A_KC, B_KC, 128, 256, 32, 2, 2, 3, 2>(p, stream);
       case kCfg256x128: return launch_bf16<A_KC, B_KC, 256, 128, 32, 2, 2, VEC, 2>(p, stream);
       case kCfg128x256: return launch_bf16<A_KC, B_KC, 128, 256, 32, 2, 2, VEC, 2>(p, stream);
       case kCfg128x128: return launch_bf16<A_KC, B_KC, 128, 128, 32, 2, 2, VEC, 2>(p, stream);

@@ -116,10 +116,13 @@ struct DmaLoader {
   using T = DmaTile<ES, KC, BMN, BK>;
   static constexpr int JB = T::BLOCKS / NW;
   static_assert(T::BLOCKS % NW == 0, "blocks split evenly over the waves");
-  uint32_t off[JB];  // byte offset from the stage's tile origin in global memory
-  int row[JB], col[JB];
+  // byte offset of the lane's chunk from the stage's tile origin in global
+  // memory, or kOOB (reads zero) where its m / n lies past the matrix edge
+  uint32_t off[JB];
+  int kx[JB];  // the chunk's k within the stage (its column if K-contiguous, else its row)
 
-  __device__ __forceinline__ void init(int wave, int lane, int64_t ld) {
+  // mn_left: rows of A (columns of B) from the block's tile origin on
+  __device__ __forceinline__ void init(int wave, int lane, int64_t ld, int64_t mn_left) {
 #pragma unroll
     for (int j = 0; j < JB; ++j) {
       const int b = wave + NW * j;
@@ -127,29 +130,37 @@ struct DmaLoader {
       const int r = byte / T::RB;
       const int pchunk = (byte % T::RB) / 16;
       const int c = (pchunk ^ T::swz(r)) * T::EPC;
-      row[j] = r;
-      col[j] = c;
-      off[j] = (uint32_t)(((int64_t)r * ld + c) * ES);
+      const int mn = KC ? r : c;
+      kx[j] = KC ? c : r;
+      off[j] = mn < mn_left ? (uint32_t)(((int64_t)r * ld + c) * ES) : kOOB;
     }
   }
-  // base: global element (row 0, col 0) of this stage's tile; lds: the tile's
-  // LDS origin. Out-of-range rows / columns read as zero.
-  __device__ __forceinline__ void issue(const char* base, int64_t rows_left, int64_t cols_left,
-                                        char* lds, int wave) const {
-    const __amdgpu_buffer_rsrc_t r = make_rsrc(uniform_ptr(base));
-    const int rl = rows_left < T::ROWS ? (int)rows_left : T::ROWS;
-    const int cl = cols_left < (T::RB / ES) ? (int)cols_left : (T::RB / ES);
-    const uint32_t lds0 = lds_byte_addr(lds);
-#pragma unroll
-    for (int j = 0; j < JB; ++j) {
-      const bool ok = row[j] < rl && col[j] < cl;
-      dma16(r, ok ? off[j] : kOOB, lds0 + 1024 * (wave + NW * j));
-    }
+  // What one stage's loads of this operand need, computed once per stage:
+  // the buffer descriptor, the k left in range (BK for a whole stage), the
+  // LDS origin.
+  struct Plan {
+    __amdgpu_buffer_rsrc_t r;
+    int kl;
+    uint32_t lds0;
+  };
+  // base: the stage's tile origin in global memory; lds: the tile's LDS origin
+  __device__ __forceinline__ Plan plan(const char* base, int64_t k_left, char* lds) const {
+    Plan q;
+    q.r = make_rsrc(uniform_ptr(base));
+    q.kl = k_left < BK ? (int)k_left : BK;
+    q.lds0 = lds_byte_addr(lds);
+    return q;
+  }
+  // The j-th of this wave's JB loads of the stage; chunks past the K tail
+  // read as zero.
+  __device__ __forceinline__ void issue_one(const Plan& q, int j, int wave) const {
+    dma16(q.r, kx[j] < q.kl ? off[j] : kOOB, q.lds0 + 1024 * (wave + NW * j));
   }
 };
 
 // Fragment loads and MFMAs of one k-step, split so that the next k-step's
-// fragments (across stages, too) load while the current k-step multiplies.
+// fragments load while the current k-step multiplies, and the MFMAs in
+// chunks between which the kernel places its loads.
 template <typename T, bool A_KC, bool B_KC, int TM, int TN, int BK, int BM, int BN>
 struct DmaMma;
 
@@ -185,14 +196,15 @@ struct DmaMma<float, A_KC, B_KC, TM, TN, BK, BM, BN> {
 #pragma unroll
     for (int i = 0; i < TN; ++i) frag<B_KC, BN, TN>(Bs, bn + i * 32, g, lane, f.b, i);
   }
-  static __device__ __forceinline__ void compute(const Frags& f, f32x16 (&acc)[TM][TN]) {
+  // a k-step's MFMAs in 4 chunks: chunk j is MFMA step j of every tile
+  static constexpr int CHUNKS = 4;
+  static __device__ __forceinline__ void compute_chunk(const Frags& f, f32x16 (&acc)[TM][TN],
+                                                       int j) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int q = 0; q < TN; ++q)
-          acc[i][q] = __builtin_amdgcn_mfma_f32_32x32x2f32(f.b[j][q], f.a[j][i], acc[i][q], 0, 0, 0);
+      for (int q = 0; q < TN; ++q)
+        acc[i][q] = __builtin_amdgcn_mfma_f32_32x32x2f32(f.b[j][q], f.a[j][i], acc[i][q], 0, 0, 0);
   }
 };
 
@@ -236,19 +248,20 @@ struct DmaMma<__bf16, A_KC, B_KC, TM, TN, BK, BM, BN> {
 #pragma unroll
     for (int i = 0; i < TN; ++i) f.b[i] = frag<B_KC, BN>(Bs, bn + i * 32, k0, lane);
   }
-  static __device__ __forceinline__ void compute(const Frags& f, f32x16 (&acc)[TM][TN]) {
+  // a k-step's MFMAs in TM chunks: chunk i is row i of the wave's tiles
+  static constexpr int CHUNKS = TM;
+  static __device__ __forceinline__ void compute_chunk(const Frags& f, f32x16 (&acc)[TM][TN],
+                                                       int i) {
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int q = 0; q < TN; ++q)
-        acc[i][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, f.b[q]),
-                                                             __builtin_bit_cast(bf16x8, f.a[i]),
-                                                             acc[i][q], 0, 0, 0);
+    for (int q = 0; q < TN; ++q)
+      acc[i][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, f.b[q]),
+                                                           __builtin_bit_cast(bf16x8, f.a[i]),
+                                                           acc[i][q], 0, 0, 0);
   }
 };
 
 template <typename T, bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int WGN, int NS,
-          int ISSUE_AT,
+          int DMA_G0, int DMA_GS,
           int WAVES_PER_EU>
 __global__ __launch_bounds__(WGM * WGN * 64)
 __attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
@@ -258,7 +271,6 @@ void gemm_dma_kernel(const GemmParams p) {
   constexpr int WTM = BM / WGM, WTN = BN / WGN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
   static_assert(NS >= 2 && NS <= 5, "a ring of two to five stages");
-  static_assert(ISSUE_AT >= 0 && ISSUE_AT < BK / (sizeof(T) == 4 ? 8 : 16), "issue point is a k-step");
   using LA = DmaLoader<ES, A_KC, BM, BK, NW>;
   using LB = DmaLoader<ES, B_KC, BN, BK, NW>;
   constexpr int A_BYTES = LA::T::BYTES, B_BYTES = LB::T::BYTES;
@@ -311,8 +323,8 @@ void gemm_dma_kernel(const GemmParams p) {
 
   LA la;
   LB lb;
-  la.init(wave, lane, p.lda);
-  lb.init(wave, lane, p.ldb);
+  la.init(wave, lane, p.lda, p.M - m0);
+  lb.init(wave, lane, p.ldb, p.N - n0);
 
   // issue cursor: (summed batch index r, k tile kt) of the next stage to load
   int64_t cur_r = KS > 0 ? st0 / KS : 0, cur_kt = KS > 0 ? st0 % KS : 0;
@@ -328,20 +340,44 @@ void gemm_dma_kernel(const GemmParams p) {
     }
   };
   if (S > 0 && p.nred > 0) red_offsets(cur_r);
-  auto issue_next = [&](int slot) {
+  // tile origins of the next stage to load, advanced by one K-stage per
+  // load; recomputed only where the summed batch index moves on
+  const int64_t a_step = (A_KC ? (int64_t)BK : (int64_t)BK * p.lda) * ES;
+  const int64_t b_step = (B_KC ? (int64_t)BK : (int64_t)BK * p.ldb) * ES;
+  const char* a_nxt = A;
+  const char* b_nxt = B;
+  int64_t k_left = 0;
+  auto seek = [&]() {
     const int64_t k0 = cur_kt * BK;
-    const char* Ar = A + ra_off * ES;
-    const char* Br = B + rb_off * ES;
+    a_nxt = A + (ra_off + (A_KC ? m0 * p.lda + k0 : k0 * p.lda + m0)) * ES;
+    b_nxt = B + (rb_off + (B_KC ? n0 * p.ldb + k0 : k0 * p.ldb + n0)) * ES;
+    k_left = p.K - k0;
+  };
+  if (S > 0) seek();
+  // plans of the next stage's loads (into LDS slot `slot`); advances the cursor
+  typename LA::Plan pa;
+  typename LB::Plan pb;
+  auto plan_next = [&](int slot) {
     char* dst = lds + slot * STAGE;
-    if (A_KC) la.issue(Ar + (m0 * p.lda + k0) * ES, p.M - m0, p.K - k0, dst, wave);
-    else la.issue(Ar + (k0 * p.lda + m0) * ES, p.K - k0, p.M - m0, dst, wave);
-    if (B_KC) lb.issue(Br + (n0 * p.ldb + k0) * ES, p.N - n0, p.K - k0, dst + A_BYTES, wave);
-    else lb.issue(Br + (k0 * p.ldb + n0) * ES, p.K - k0, p.N - n0, dst + A_BYTES, wave);
+    pa = la.plan(a_nxt, k_left, dst);
+    pb = lb.plan(b_nxt, k_left, dst + A_BYTES);
     if (++cur_kt == KS) {
       cur_kt = 0;
       ++cur_r;
-      if (cur_r < p.red_count) red_offsets(cur_r);
+      if (cur_r < p.red_count) {
+        red_offsets(cur_r);
+        seek();
+      }
+    } else {
+      a_nxt += a_step;
+      b_nxt += b_step;
+      k_left -= BK;
     }
+  };
+  // the j-th (of L) load of the planned stage: A's first, then B's
+  auto issue_one = [&](int j) {
+    if (j < LA::JB) la.issue_one(pa, j, wave);
+    else lb.issue_one(pb, j - LA::JB, wave);
   };
 
   f32x16 acc[TM][TN];
@@ -356,10 +392,21 @@ void gemm_dma_kernel(const GemmParams p) {
 
   // prologue: stages 0 .. NS-2 in flight
 #pragma unroll
-  for (int q = 0; q < NS - 1; ++q)
-    if (q < S) issue_next(q);
+  for (int q = 0; q < NS - 1; ++q) {
+    if (q < S) {
+      plan_next(q);
+#pragma unroll
+      for (int j = 0; j < L; ++j) issue_one(j);
+    }
+  }
 
-  for (int s = 0; s < S; ++s) {
+  constexpr int CHUNKS = Mma::CHUNKS;
+  static_assert(DMA_G0 >= 0 && DMA_GS >= 1 && DMA_G0 < Mma::KSTEPS * CHUNKS, "issue points");
+  // issue points: chunks DMA_G0, DMA_G0 + DMA_GS, ... of the stage; PER loads at each
+  constexpr int POINTS = (Mma::KSTEPS * CHUNKS - DMA_G0 + DMA_GS - 1) / DMA_GS;
+  constexpr int PER = (L + POINTS - 1) / POINTS;
+  // one stage; more: the loads of stage s+NS-1 go out during it
+  auto run_stage = [&](int s, bool more) {
     // this wave's loads of stage s have landed once at most `younger` later
     // stages (of L loads each) are still in flight; the barrier then makes
     // every wave's loads visible and frees the slot stage s-1 used
@@ -378,14 +425,27 @@ void gemm_dma_kernel(const GemmParams p) {
 #pragma unroll
     for (int ks = 0; ks < Mma::KSTEPS; ++ks) {
       if (ks + 1 < Mma::KSTEPS) Mma::load(st, st + A_BYTES, am, bn, lane, ks + 1, nxt);
-      Mma::compute(cur, acc);
-      // the next stage's loads go out behind the first k-step's MFMAs, so
-      // that their address arithmetic and issue overlap matrix work
-      if (ks == ISSUE_AT && s + NS - 1 < S) issue_next((s + NS - 1) % NS);
+#pragma unroll
+      for (int c = 0; c < CHUNKS; ++c) {
+        Mma::compute_chunk(cur, acc, c);
+        if (more) {
+          // the next stage's L loads go out PER at a time after every
+          // DMA_GS-th chunk of MFMAs from chunk DMA_G0 on, so that no wave
+          // stalls on a burst of loads the memory pipeline cannot take at once
+          const int g = ks * CHUNKS + c;
+          if (g >= DMA_G0 && (g - DMA_G0) % DMA_GS == 0 && (g - DMA_G0) / DMA_GS * PER < L) {
+            if (g == DMA_G0) plan_next((s + NS - 1) % NS);
+            const int j0 = (g - DMA_G0) / DMA_GS * PER;
+#pragma unroll
+            for (int j = j0; j < j0 + PER && j < L; ++j) issue_one(j);
+          }
+        }
+      }
       cur = nxt;
     }
     __asm__ __volatile__("" ::: "memory");
-  }
+  };
+  for (int s = 0; s < S; ++s) run_stage(s, s + NS - 1 < S);
 
   // ---- epilogue (as in gemm_kernel): lane holds C[m][n0' + 8g + 4h + 0..3]
   const bool to_partial = p.splits > 1;

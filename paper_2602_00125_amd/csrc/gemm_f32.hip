@@ -27,7 +27,7 @@ static hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
   const int64_t blocks = (int64_t)q.tiles_m * q.tiles_n * p.keep_count * p.splits;
   if (blocks <= 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((gemm::gemm_dma_kernel<float, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 0, WPE>),
+  hipLaunchKernelGGL((gemm::gemm_dma_kernel<float, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 1, 1, WPE>),
                      dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
   return hipGetLastError();
 }
@@ -42,6 +42,8 @@ static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream
     switch (cfg) {
       case kCfgDma256x256: return launch_dma<A_KC, B_KC, 256, 256, 32, 2, 4, 2, 2>(p, stream);
       case kCfgDma256x256w4: return launch_dma<A_KC, B_KC, 256, 256, 32, 2, 2, 2, 1>(p, stream);
+      case kCfgDma256x128: return launch_dma<A_KC, B_KC, 256, 128, 16, 2, 2, 3, 2>(p, stream);
+      case kCfgDma128x256: return launch_dma<A_KC, B_KC, 128, 256, 16, 2, 2, 3, 2>(p, stream);
       case kCfg256x256: return launch_f32<A_KC, B_KC, 256, 256, 16, 2, 2, VEC, 1>(p, stream);
       case kCfg256x256x64w8: return launch_f32<A_KC, B_KC, 256, 256, 32, 2, 4, VEC, 2>(p, stream);
       case kCfg256x128: return launch_f32<A_KC, B_KC, 256, 128, 16, 2, 2, VEC, 2>(p, stream);
@@ -55,16 +57,16 @@ static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream
 int gemm_tile_m(int cfg) {
   switch (cfg) {
     case kCfg256x256: case kCfg256x128: case kCfg256x256x64w8: case kCfgDma256x256:
-    case kCfgDma256x256w4: return 256;
-    case kCfg128x256: case kCfg128x128: return 128;
+    case kCfgDma256x256w4: case kCfgDma256x128: return 256;
+    case kCfg128x256: case kCfg128x128: case kCfgDma128x256: return 128;
     default: return 64;
   }
 }
 int gemm_tile_n(int cfg) {
   switch (cfg) {
     case kCfg256x256: case kCfg128x256: case kCfg256x256x64w8: case kCfgDma256x256:
-    case kCfgDma256x256w4: return 256;
-    case kCfg256x128: case kCfg128x128: return 128;
+    case kCfgDma256x256w4: case kCfgDma128x256: return 256;
+    case kCfg256x128: case kCfg128x128: case kCfgDma256x128: return 128;
     default: return 64;
   }
 }

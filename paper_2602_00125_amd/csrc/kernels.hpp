@@ -8,9 +8,10 @@
 
 namespace mt {
 
-// GEMM tile configurations (BM x BN; BK = 16 fp32 / 32 bf16; 4 waves per
-// block), plus a 256x256 configuration with 8 waves and BK = 32 fp32 / 64
-// bf16.
+// GEMM tile configurations: register-staged tiles (BM x BN; BK = 16 fp32 /
+// 32 bf16; 4 waves per block), a register-staged 256x256 tile with 8 waves
+// and BK = 32 fp32 / 64 bf16, and tiles whose operands stream straight into
+// an LDS ring (gemm_dma.hpp).
 enum GemmCfg {
   kCfg256x256 = 0,
   kCfg256x128 = 1,
@@ -18,8 +19,11 @@ enum GemmCfg {
   kCfg128x128 = 3,
   kCfg64x64 = 4,
   kCfg256x256x64w8 = 5,
-  kCfgDma256x256 = 6,   // 256x256, 8 waves, tiles loaded straight into a 4-stage LDS ring
-  kCfgDma256x256w4 = 7  // the same with 4 waves (128x128 per wave)
+  kCfgDma256x256 = 6,    // 256x256, 8 waves, BK = 32 / 64, 2-stage ring (128 KB), 1 block per CU
+  kCfgDma256x256w4 = 7,  // the same with 4 waves (128x128 per wave)
+  kCfgDma256x128 = 8,    // 256x128, 4 waves, BK = 16 / 32, 3-stage ring (72 KB), 2 blocks per CU
+  kCfgDma128x256 = 9,    // 128x256, likewise
+  kNumGemmCfg = 10
 };
 int gemm_tile_m(int cfg);
 int gemm_tile_n(int cfg);

@@ -69,7 +69,7 @@ def test_linear_64x32x128_workload():
     check_full(out, oracle_full(inp))
 
 
-@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4, 5, 6, 7])
+@pytest.mark.parametrize("cfg", list(range(10)))
 @pytest.mark.parametrize("vec1", [0, 1])
 def test_linear_every_tile_config(cfg, vec1):
     inp = wl.linear(520, 392, 264, seed=11).make()
