@@ -29,12 +29,13 @@
 // the swizzle places at its LDS slot.
 //
 // Pipeline per stage s: wait until this wave's loads of stage s have landed
-// (s_waitcnt vmcnt with the number of younger stages in flight), barrier
+// (s_waitcnt vmcnt with the NS-2 younger stages still in flight), barrier
 // (every wave's loads of stage s landed; every wave finished reading stage
 // s-1), then the k-steps of stage s, each k-step's fragments read from LDS
 // while the previous k-step's MFMAs run. The loads of stage s+NS-1 (into
-// the slot of stage s-1) go out after the first k-step's MFMAs are issued,
-// so their address arithmetic overlaps matrix work. The barrier is a bare
+// the slot of stage s-1) go out one at a time between chunks of MFMAs. In
+// the last NS-1 stages those loads are empty (all out of range, zeros into
+// a dead slot), so the stage loop has no branches. The barrier is a bare
 // s_barrier: a release fence would make every wave wait for all loads in
 // flight, younger stages included.
 #pragma once
@@ -349,18 +350,24 @@ void gemm_dma_kernel(const GemmParams p) {
   int64_t k_left = 0;
   auto seek = [&]() {
     const int64_t k0 = cur_kt * BK;
-    a_nxt = A + (ra_off + (A_KC ? m0 * p.lda + k0 : k0 * p.lda + m0)) * ES;
-    b_nxt = B + (rb_off + (B_KC ? n0 * p.ldb + k0 : k0 * p.ldb + n0)) * ES;
+    a_nxt = uniform_ptr(A + (ra_off + (A_KC ? m0 * p.lda + k0 : k0 * p.lda + m0)) * ES);
+    b_nxt = uniform_ptr(B + (rb_off + (B_KC ? n0 * p.ldb + k0 : k0 * p.ldb + n0)) * ES);
     k_left = p.K - k0;
   };
   if (S > 0) seek();
   // plans of the next stage's loads (into LDS slot `slot`); advances the cursor
   typename LA::Plan pa;
   typename LB::Plan pb;
+  // Stages past the last (planned while the final NS-1 stages compute) load
+  // nothing: every chunk is out of range and reads zero into a slot no wave
+  // reads again, so the loop issues the same loads in every stage, unbranched.
+  int planned = 0;
   auto plan_next = [&](int slot) {
     char* dst = lds + slot * STAGE;
-    pa = la.plan(a_nxt, k_left, dst);
-    pb = lb.plan(b_nxt, k_left, dst + A_BYTES);
+    const int64_t kl = planned < S ? k_left : 0;
+    ++planned;
+    pa = la.plan(a_nxt, kl, dst);
+    pb = lb.plan(b_nxt, kl, dst + A_BYTES);
     if (++cur_kt == KS) {
       cur_kt = 0;
       ++cur_r;
@@ -393,11 +400,9 @@ void gemm_dma_kernel(const GemmParams p) {
   // prologue: stages 0 .. NS-2 in flight
 #pragma unroll
   for (int q = 0; q < NS - 1; ++q) {
-    if (q < S) {
-      plan_next(q);
+    plan_next(q);
 #pragma unroll
-      for (int j = 0; j < L; ++j) issue_one(j);
-    }
+    for (int j = 0; j < L; ++j) issue_one(j);
   }
 
   constexpr int CHUNKS = Mma::CHUNKS;
@@ -405,21 +410,15 @@ void gemm_dma_kernel(const GemmParams p) {
   // issue points: chunks DMA_G0, DMA_G0 + DMA_GS, ... of the stage; PER loads at each
   constexpr int POINTS = (Mma::KSTEPS * CHUNKS - DMA_G0 + DMA_GS - 1) / DMA_GS;
   constexpr int PER = (L + POINTS - 1) / POINTS;
-  // one stage; more: the loads of stage s+NS-1 go out during it
-  auto run_stage = [&](int s, bool more) {
-    // this wave's loads of stage s have landed once at most `younger` later
-    // stages (of L loads each) are still in flight; the barrier then makes
-    // every wave's loads visible and frees the slot stage s-1 used
-    {
-      const int issued = (s + NS - 2) < (S - 1) ? (s + NS - 2) : (S - 1);
-      const int younger = issued - s;
-      if (NS >= 5 && younger >= 3) wait_vmcnt<3 * L>();
-      else if (NS >= 4 && younger >= 2) wait_vmcnt<2 * L>();
-      else if (NS >= 3 && younger == 1) wait_vmcnt<L>();
-      else wait_vmcnt<0>();
-      __builtin_amdgcn_s_barrier();
-      __asm__ __volatile__("" ::: "memory");
-    }
+  // one stage; the loads of stage s+NS-1 go out during it
+  auto run_stage = [&](int s) {
+    // stages 0 .. s+NS-2 have been issued: this wave's loads of stage s have
+    // landed once at most NS-2 later stages (of L loads each) are in flight;
+    // the barrier then makes every wave's loads visible and frees the slot
+    // stage s-1 used
+    wait_vmcnt<(NS - 2) * L>();
+    __builtin_amdgcn_s_barrier();
+    __asm__ __volatile__("" ::: "memory");
     const char* st = lds + (s % NS) * STAGE;
     Mma::load(st, st + A_BYTES, am, bn, lane, 0, cur);
 #pragma unroll
@@ -428,24 +427,27 @@ void gemm_dma_kernel(const GemmParams p) {
 #pragma unroll
       for (int c = 0; c < CHUNKS; ++c) {
         Mma::compute_chunk(cur, acc, c);
-        if (more) {
-          // the next stage's L loads go out PER at a time after every
-          // DMA_GS-th chunk of MFMAs from chunk DMA_G0 on, so that no wave
-          // stalls on a burst of loads the memory pipeline cannot take at once
-          const int g = ks * CHUNKS + c;
-          if (g >= DMA_G0 && (g - DMA_G0) % DMA_GS == 0 && (g - DMA_G0) / DMA_GS * PER < L) {
-            if (g == DMA_G0) plan_next((s + NS - 1) % NS);
-            const int j0 = (g - DMA_G0) / DMA_GS * PER;
+        // the next stage's L loads go out PER at a time after every
+        // DMA_GS-th chunk of MFMAs from chunk DMA_G0 on, so that no wave
+        // stalls on a burst of loads the memory pipeline cannot take at once
+        const int g = ks * CHUNKS + c;
+        if (g >= DMA_G0 && (g - DMA_G0) % DMA_GS == 0 && (g - DMA_G0) / DMA_GS * PER < L) {
+          if (g == DMA_G0) plan_next((s + NS - 1) % NS);
+          const int j0 = (g - DMA_G0) / DMA_GS * PER;
 #pragma unroll
-            for (int j = j0; j < j0 + PER && j < L; ++j) issue_one(j);
-          }
+          for (int j = j0; j < j0 + PER && j < L; ++j) issue_one(j);
         }
+        // keep each chunk's MFMAs and loads where they are: left to itself
+        // the scheduler gathers the loads into bursts again
+        __builtin_amdgcn_sched_barrier(0);
       }
       cur = nxt;
     }
     __asm__ __volatile__("" ::: "memory");
   };
-  for (int s = 0; s < S; ++s) run_stage(s, s + NS - 1 < S);
+  for (int s = 0; s < S; ++s) run_stage(s);
+  // the empty loads of the stages past the last land before the wave ends
+  wait_vmcnt<0>();
 
   // ---- epilogue (as in gemm_kernel): lane holds C[m][n0' + 8g + 4h + 0..3]
   const bool to_partial = p.splits > 1;
