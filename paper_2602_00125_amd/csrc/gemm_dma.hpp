@@ -144,18 +144,25 @@ struct DmaLoader {
     int kl;
     uint32_t lds0;
   };
-  // base: the stage's tile origin in global memory; lds: the tile's LDS origin
+  // base: the stage's tile origin in global memory; lds: the tile's LDS
+  // origin. An empty stage (k_left <= 0) gets a descriptor of zero records:
+  // all its loads read zero without touching memory.
   __device__ __forceinline__ Plan plan(const char* base, int64_t k_left, char* lds) const {
     Plan q;
-    q.r = make_rsrc(uniform_ptr(base));
+    q.r = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(uniform_ptr(base)), (short)0,
+                                            k_left > 0 ? 0x7fffffff : 0, kRsrcWord3);
     q.kl = k_left < BK ? (int)k_left : BK;
     q.lds0 = lds_byte_addr(lds);
     return q;
   }
-  // The j-th of this wave's JB loads of the stage; chunks past the K tail
-  // read as zero.
+  // The j-th of this wave's JB loads of the stage. KTAIL (K not a multiple
+  // of BK): chunks past the K tail read as zero; otherwise every stage is
+  // whole and the per-lane test is left out (vector instructions between
+  // the MFMAs cost matrix throughput).
+  template <bool KTAIL>
   __device__ __forceinline__ void issue_one(const Plan& q, int j, int wave) const {
-    dma16(q.r, kx[j] < q.kl ? off[j] : kOOB, q.lds0 + 1024 * (wave + NW * j));
+    const uint32_t o = KTAIL ? (kx[j] < q.kl ? off[j] : kOOB) : off[j];
+    dma16(q.r, o, q.lds0 + 1024 * (wave + NW * j));
   }
 };
 
@@ -262,7 +269,7 @@ struct DmaMma<__bf16, A_KC, B_KC, TM, TN, BK, BM, BN> {
 };
 
 template <typename T, bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int WGN, int NS,
-          int DMA_G0, int DMA_GS,
+          int DMA_G0, int DMA_GS, bool KTAIL,
           int WAVES_PER_EU>
 __global__ __launch_bounds__(WGM * WGN * 64)
 __attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
@@ -383,8 +390,8 @@ void gemm_dma_kernel(const GemmParams p) {
   };
   // the j-th (of L) load of the planned stage: A's first, then B's
   auto issue_one = [&](int j) {
-    if (j < LA::JB) la.issue_one(pa, j, wave);
-    else lb.issue_one(pb, j - LA::JB, wave);
+    if (j < LA::JB) la.template issue_one<KTAIL>(pa, j, wave);
+    else lb.template issue_one<KTAIL>(pb, j - LA::JB, wave);
   };
 
   f32x16 acc[TM][TN];

@@ -27,8 +27,13 @@ static hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
   const int64_t blocks = (int64_t)q.tiles_m * q.tiles_n * p.keep_count * p.splits;
   if (blocks <= 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((gemm::gemm_dma_kernel<float, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 1, 1, WPE>),
-                     dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
+  // the per-load K-tail test only where K is not a whole number of stages
+  if (p.K % BK != 0)
+    hipLaunchKernelGGL((gemm::gemm_dma_kernel<float, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 1, 1, true, WPE>),
+                       dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
+  else
+    hipLaunchKernelGGL((gemm::gemm_dma_kernel<float, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 1, 1, false, WPE>),
+                       dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
   return hipGetLastError();
 }
 

@@ -71,8 +71,10 @@ def test_bf16_linear_small_and_ragged(M, N, K):
 
 @pytest.mark.parametrize("cfg", list(range(10)))
 @pytest.mark.parametrize("vec1", [0, 1])
-def test_bf16_every_tile_config(cfg, vec1):
-    inp = make(520, 392, 264, seed=17)
+@pytest.mark.parametrize("shape", [(520, 392, 264), (576, 320, 256)])
+def test_bf16_every_tile_config(cfg, vec1, shape):
+    # K tails in every product, then none (see the fp32 test of the same name)
+    inp = make(*shape, seed=17)
     b.debug_set("cfg", cfg)
     b.debug_set("vec1", vec1)
     try:

@@ -71,8 +71,12 @@ def test_linear_64x32x128_workload():
 
 @pytest.mark.parametrize("cfg", list(range(10)))
 @pytest.mark.parametrize("vec1", [0, 1])
-def test_linear_every_tile_config(cfg, vec1):
-    inp = wl.linear(520, 392, 264, seed=11).make()
+@pytest.mark.parametrize("shape", [(520, 392, 264), (576, 320, 256)])
+def test_linear_every_tile_config(cfg, vec1, shape):
+    # (520, 392, 264): no product's K is a whole number of K-stages (K tails);
+    # (576, 320, 256): every product's K is (the tail-free kernel builds),
+    # with M and N still cutting the tiles
+    inp = wl.linear(*shape, seed=11).make()
     b.debug_set("cfg", cfg)
     b.debug_set("vec1", vec1)
     try:
