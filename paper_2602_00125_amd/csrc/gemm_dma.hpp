@@ -71,6 +71,12 @@ __device__ __forceinline__ const char* uniform_ptr(const char* p) {
   return (const char*)(uintptr_t)(((uint64_t)hi << 32) | lo);
 }
 
+__device__ __forceinline__ int64_t uniform_i64(int64_t v) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 __device__ __forceinline__ uint32_t lds_byte_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
 }
@@ -145,13 +151,14 @@ struct DmaLoader {
     uint32_t lds0;
   };
   // base: the stage's tile origin in global memory; lds: the tile's LDS
-  // origin. An empty stage (k_left <= 0) gets a descriptor of zero records:
-  // all its loads read zero without touching memory.
-  __device__ __forceinline__ Plan plan(const char* base, int64_t k_left, char* lds) const {
+  // origin. A stage that is not live (past the last) gets a descriptor of
+  // zero records: all its loads read zero without touching memory.
+  __device__ __forceinline__ Plan plan(const char* base, int64_t k_left, char* lds,
+                                       bool live) const {
     Plan q;
-    q.r = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(uniform_ptr(base)), (short)0,
-                                            k_left > 0 ? 0x7fffffff : 0, kRsrcWord3);
-    q.kl = k_left < BK ? (int)k_left : BK;
+    q.r = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), (short)0,
+                                            live ? 0x7fffffff : 0, kRsrcWord3);
+    q.kl = !live ? 0 : k_left < BK ? (int)k_left : BK;
     q.lds0 = lds_byte_addr(lds);
     return q;
   }
@@ -334,8 +341,10 @@ void gemm_dma_kernel(const GemmParams p) {
   la.init(wave, lane, p.lda, p.M - m0);
   lb.init(wave, lane, p.ldb, p.N - n0);
 
-  // issue cursor: (summed batch index r, k tile kt) of the next stage to load
-  int64_t cur_r = KS > 0 ? st0 / KS : 0, cur_kt = KS > 0 ? st0 % KS : 0;
+  // issue cursor: (summed batch index r, k tile kt) of the next stage to
+  // load, wave-uniform (scalar registers)
+  int64_t cur_r = uniform_i64(KS > 0 ? st0 / KS : 0);
+  int64_t cur_kt = uniform_i64(KS > 0 ? st0 % KS : 0);
   int64_t ra_off = 0, rb_off = 0;
   auto red_offsets = [&](int64_t r) {
     ra_off = 0;
@@ -359,7 +368,7 @@ void gemm_dma_kernel(const GemmParams p) {
     const int64_t k0 = cur_kt * BK;
     a_nxt = uniform_ptr(A + (ra_off + (A_KC ? m0 * p.lda + k0 : k0 * p.lda + m0)) * ES);
     b_nxt = uniform_ptr(B + (rb_off + (B_KC ? n0 * p.ldb + k0 : k0 * p.ldb + n0)) * ES);
-    k_left = p.K - k0;
+    k_left = uniform_i64(p.K - k0);
   };
   if (S > 0) seek();
   // plans of the next stage's loads (into LDS slot `slot`); advances the cursor
@@ -371,10 +380,10 @@ void gemm_dma_kernel(const GemmParams p) {
   int planned = 0;
   auto plan_next = [&](int slot) {
     char* dst = lds + slot * STAGE;
-    const int64_t kl = planned < S ? k_left : 0;
+    const bool live = planned < S;
     ++planned;
-    pa = la.plan(a_nxt, kl, dst);
-    pb = lb.plan(b_nxt, kl, dst + A_BYTES);
+    pa = la.plan(a_nxt, k_left, dst, live);
+    pb = lb.plan(b_nxt, k_left, dst + A_BYTES, live);
     if (++cur_kt == KS) {
       cur_kt = 0;
       ++cur_r;
