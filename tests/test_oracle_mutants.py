@@ -50,3 +50,48 @@ def test_pins_catch_mutant(tmp_path, name, old, new):
                         os.path.join(HERE, "test_oracle.py")], cwd=ROOT, env=env,
                        capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the oracle pins:\n{r.stdout[-2000:]}"
+
+
+# planted mistakes in oracle/nn.py, caught by test_oracle_nn.py
+NN_SRC = os.path.join(ROOT, "oracle", "nn.py")
+MUTANTS_NN = [
+    ("gelu_tanh_approximation", "        return z * normal_cdf(z)\n",
+     "        return 0.5 * z * (1.0 + np.tanh(0.7978845608028654 * (z + 0.044715 * z ** 3)))\n"),
+    ("gelu_grad_drops_pdf_term", "        return normal_cdf(z) + z * normal_pdf(z)\n",
+     "        return normal_cdf(z)\n"),
+    ("relu_grad_one_at_zero", "        return (z > 0).astype(np.float64)\n",
+     "        return (z >= 0).astype(np.float64)\n"),
+    ("sigmoid_grad_sign", "        return s * (1.0 - s)\n", "        return s * (1.0 + s)\n"),
+    ("tanh_grad_not_squared", "        return 1.0 - t * t\n", "        return 1.0 - t\n"),
+    ("act_bwd_evaluates_grad_at_output", "    dZ = dH * act_grad(kind, Z)\n",
+     "    dZ = dH * act_grad(kind, act(kind, Z))\n"),
+    ("db_skips_first_row", "    for m in range(Z.shape[0]):   # rows in ascending order\n",
+     "    for m in range(1, Z.shape[0]):\n"),
+    ("mse_sum_not_mean", "    L = float(np.sum(d * d)) / N if N else 0.0\n",
+     "    L = float(np.sum(d * d)) if N else 0.0\n"),
+    ("mse_grad_missing_two", "    dP = 2.0 * d / N if N else d.copy()\n", "    dP = d / N if N else d.copy()\n"),
+    ("sgd_weight_decay_sign", "    v_new = momentum * v + g + weight_decay * theta\n",
+     "    v_new = momentum * v + g - weight_decay * theta\n"),
+    ("sgd_steps_with_old_velocity", "    theta_new = theta - lr * v_new\n", "    theta_new = theta - lr * v\n"),
+    ("adam_no_first_debias", "    bc1 = 1.0 - beta1 ** t\n", "    bc1 = 1.0\n"),
+    ("adam_eps_inside_root", "    denom = np.sqrt(vhat) + eps\n", "    denom = np.sqrt(vhat + eps)\n"),
+    ("rmsprop_eps_outside_root", "    scale = 1.0 / np.sqrt(v_new + eps)\n",
+     "    scale = 1.0 / (np.sqrt(v_new) + eps)\n"),
+    ("rmsprop_average_weights_swapped", "    v_new = alpha * v + (1.0 - alpha) * g * g\n",
+     "    v_new = (1.0 - alpha) * v + alpha * g * g\n"),
+    ("mlp_dW1_skips_activation", "    dW1, _ = _dense.linear_bwd_dw(dZ1, X)\n",
+     "    dW1, _ = _dense.linear_bwd_dw(dH1, X)\n"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS_NN, ids=[m[0] for m in MUTANTS_NN])
+def test_nn_pins_catch_mutant(tmp_path, name, old, new):
+    src = open(NN_SRC).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} not unique/found"
+    mutated = tmp_path / "nn_mut.py"
+    mutated.write_text(src.replace(old, new))
+    env = dict(os.environ, MT_ORACLE_NN_OVERRIDE=str(mutated), OMP_NUM_THREADS="2")
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(HERE, "test_oracle_nn.py")], cwd=ROOT, env=env,
+                       capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"mutant {name} survived the oracle pins:\n{r.stdout[-2000:]}"
