@@ -112,6 +112,95 @@ mt_status mt_linear_bwd_workspace(const mt_tensor* x, const mt_tensor* w, const 
                                   const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db,
                                   size_t* bytes);
 
+/* ------------------------------------------ dense layer + nonlinearity
+ * Nonlinearities of Sec. 3.3 ("Nonlinearities"): ReLU, Sigmoid, Tanh, GELU
+ * (z Phi(z) with the standard normal CDF Phi, not its tanh approximation).
+ * Their derivatives: ReLU 1{z > 0}, Sigmoid s (1 - s), Tanh 1 - tanh^2,
+ * GELU Phi(z) + z phi(z). Evaluated in fp32 with the device library's
+ * expf / tanhf / erff.
+ */
+#define MT_ACT_NONE 0
+#define MT_ACT_RELU 1
+#define MT_ACT_SIGMOID 2
+#define MT_ACT_TANH 3
+#define MT_ACT_GELU 4
+
+/* mt_linear_act_fwd: y = act(Z), Z = X W^T + 1 b^T (Eq. (5) followed by a
+ * nonlinearity), fused into the product's epilogue: the biased accumulators
+ * go through act in registers and Z is never re-read.
+ *   x, w, b, y as for mt_linear_fwd; act: one of MT_ACT_*;
+ *   z [M, N] f32 or NULL: receives the pre-activation Z (the pullback of
+ *   act needs it; mt_act_bwd takes it). Any row pitch, inner dim contiguous.
+ * Errors as mt_linear_fwd, plus MT_ERR_INVALID for an unknown act and
+ * MT_ERR_ALIAS when z overlaps an input or y.
+ */
+mt_status mt_linear_act_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* b,
+                            int32_t act, const mt_tensor* z, const mt_tensor* y, void* stream);
+
+/* mt_act_bwd: the pullback of y = act(z) (chain rule, Sec. 3.2 Eq. (3)), with
+ * the bias gradient of the dense layer before it folded into the same pass:
+ *   dz = dy * act'(z)                      elementwise
+ *   db = 1^T dz  (sum over rows)           the add pullback through the
+ *                                          broadcast bias (Sec. 3.1, 3.2)
+ *   z  [M, N] f32 (the saved pre-activation)
+ *   dy [M, N] f32 or bf16; dz [M, N] the same dtype as dy (bf16: rounded to
+ *   nearest even from the fp32 product); db [N] f32 or NULL, summed from the
+ *   fp32 products before any rounding.
+ * Matrices: any row pitch, inner dim contiguous. flags: MT_ACCUMULATE adds
+ * into dz and db. ws: optional (mt_act_bwd_workspace), row-slice sums of db.
+ * dz then feeds mt_linear_bwd as its dy, with db = NULL there.
+ */
+mt_status mt_act_bwd(int32_t act, const mt_tensor* z, const mt_tensor* dy, const mt_tensor* dz,
+                     const mt_tensor* db, uint32_t flags, void* ws, size_t ws_bytes,
+                     void* stream);
+mt_status mt_act_bwd_workspace(int32_t act, const mt_tensor* z, const mt_tensor* dy,
+                               const mt_tensor* dz, const mt_tensor* db, size_t* bytes);
+
+/* ------------------------------------------------------------------ loss
+ * mt_mse_loss: mean squared error (Sec. 3.3, "Losses") over all N elements
+ * and its gradient:
+ *   loss = (1/N) sum_i (pred_i - target_i)^2     (a 1-element f32 tensor, or NULL)
+ *   dpred = 2 (pred - target) / N                 (pred's shape, or NULL)
+ * pred, target, dpred: f32, contiguous, one shape. At least one output.
+ * The sum runs in fp32 per block in a fixed order, then over blocks in
+ * block order: deterministic. ws: optional (mt_mse_loss_workspace).
+ */
+mt_status mt_mse_loss(const mt_tensor* pred, const mt_tensor* target, const mt_tensor* loss,
+                      const mt_tensor* dpred, void* ws, size_t ws_bytes, void* stream);
+mt_status mt_mse_loss_workspace(const mt_tensor* pred, const mt_tensor* target, size_t* bytes);
+
+/* ------------------------------------------------------------ optimizers
+ * In-place parameter updates (Sec. 3.3, "Optimizers") for n parameter
+ * tensors at once (arrays of n descriptors; element i of each array belongs
+ * to parameter i). Every tensor is f32 and contiguous, and the tensors of
+ * one parameter share its shape. Parameters and states are read and
+ * overwritten; no updated tensor may overlap another tensor of the call.
+ * Up to 32 tensors go into one kernel launch. Arithmetic is fp32.
+ *
+ * mt_sgd_step, Eq. (9):
+ *   v <- momentum v + g + weight_decay theta;   theta <- theta - lr v
+ */
+mt_status mt_sgd_step(int32_t n, const mt_tensor* params, const mt_tensor* grads,
+                      const mt_tensor* velocity, float lr, float momentum, float weight_decay,
+                      void* stream);
+
+/* mt_adam_step, Eq. (10), at step t = `step` (>= 1, counted by the caller):
+ *   m <- b1 m + (1 - b1) g;  v <- b2 v + (1 - b2) g^2;
+ *   theta <- theta - lr (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps)
+ * The bias corrections 1 / (1 - b^t) are formed in double on the host.
+ * Needs 0 <= b1, b2 < 1 and eps >= 0 (MT_ERR_INVALID otherwise).
+ */
+mt_status mt_adam_step(int32_t n, const mt_tensor* params, const mt_tensor* grads,
+                       const mt_tensor* exp_avg, const mt_tensor* exp_avg_sq, float lr, float beta1,
+                       float beta2, float eps, int64_t step, void* stream);
+
+/* mt_rmsprop_step: an exponential average of squared gradients, the step
+ * scaled by (v + eps)^(-1/2) as the paper states it (eps inside the root):
+ *   v <- alpha v + (1 - alpha) g^2;   theta <- theta - lr g / sqrt(v + eps)
+ */
+mt_status mt_rmsprop_step(int32_t n, const mt_tensor* params, const mt_tensor* grads,
+                          const mt_tensor* sq_avg, float lr, float alpha, float eps, void* stream);
+
 /* -------------------------------------------------------------- matmul
  * mt_matmul: C = A @ B with NumPy/PyTorch matmul semantics (Eq. (1) per
  * batch element, batch dims broadcast per Sec. 3.1):

@@ -29,7 +29,10 @@ STATUS = {0: "MT_OK", 1: "MT_ERR_NULL", 2: "MT_ERR_NDIM", 3: "MT_ERR_SHAPE", 4: 
 EXPORTS = ["mt_linear_fwd", "mt_linear_bwd", "mt_linear_bwd_workspace", "mt_matmul",
            "mt_matmul_workspace",
            "mt_reduce_broadcast_grad", "mt_reduce_broadcast_grad_workspace", "mt_broadcast_shape",
-           "mt_matmul_shape", "mt_debug_set", "mt_status_str", "mt_last_error"]
+           "mt_matmul_shape", "mt_debug_set", "mt_status_str", "mt_last_error",
+           "mt_linear_act_fwd", "mt_act_bwd", "mt_act_bwd_workspace", "mt_mse_loss",
+           "mt_mse_loss_workspace", "mt_sgd_step", "mt_adam_step", "mt_rmsprop_step"]
+ACT = {"none": 0, "relu": 1, "sigmoid": 2, "tanh": 3, "gelu": 4}
 
 
 class MtTensor(ctypes.Structure):
@@ -50,15 +53,23 @@ lib.mt_reduce_broadcast_grad_workspace.argtypes = [_P, _P, ctypes.POINTER(_sz)]
 lib.mt_broadcast_shape.argtypes = [ctypes.c_int32, _I64P, ctypes.c_int32, _I64P,
                                    ctypes.POINTER(ctypes.c_int32), _I64P]
 lib.mt_matmul_shape.argtypes = lib.mt_broadcast_shape.argtypes
+lib.mt_linear_act_fwd.argtypes = [_P, _P, _P, ctypes.c_int32, _P, _P, _vp]
+lib.mt_act_bwd.argtypes = [ctypes.c_int32, _P, _P, _P, _P, _u32, _vp, _sz, _vp]
+lib.mt_act_bwd_workspace.argtypes = [ctypes.c_int32, _P, _P, _P, _P, ctypes.POINTER(_sz)]
+lib.mt_mse_loss.argtypes = [_P, _P, _P, _P, _vp, _sz, _vp]
+lib.mt_mse_loss_workspace.argtypes = [_P, _P, ctypes.POINTER(_sz)]
+_f = ctypes.c_float
+lib.mt_sgd_step.argtypes = [ctypes.c_int32, _P, _P, _P, _f, _f, _f, _vp]
+lib.mt_adam_step.argtypes = [ctypes.c_int32, _P, _P, _P, _P, _f, _f, _f, _f, ctypes.c_int64, _vp]
+lib.mt_rmsprop_step.argtypes = [ctypes.c_int32, _P, _P, _P, _f, _f, _f, _vp]
 lib.mt_debug_set.argtypes = [ctypes.c_char_p, ctypes.c_int64]
 lib.mt_status_str.argtypes = [ctypes.c_int]
 lib.mt_status_str.restype = ctypes.c_char_p
 lib.mt_last_error.argtypes = []
 lib.mt_last_error.restype = ctypes.c_char_p
-for _f in ("mt_linear_fwd", "mt_linear_bwd", "mt_linear_bwd_workspace", "mt_matmul", "mt_matmul_workspace",
-           "mt_reduce_broadcast_grad", "mt_reduce_broadcast_grad_workspace", "mt_broadcast_shape",
-           "mt_matmul_shape", "mt_debug_set"):
-    getattr(lib, _f).restype = ctypes.c_int
+for _name in EXPORTS:
+    if _name not in ("mt_status_str", "mt_last_error"):
+        getattr(lib, _name).restype = ctypes.c_int
 
 
 class MtError(RuntimeError):
@@ -176,6 +187,80 @@ def reduce_broadcast_grad(grad_out, grad_in, accumulate=False, workspace=None, s
     _check(lib.mt_reduce_broadcast_grad(_ref(desc(grad_out)), _ref(desc(grad_in)),
                                         ACCUMULATE if accumulate else 0, ptr, nbytes,
                                         _stream(stream)), "mt_reduce_broadcast_grad")
+
+
+def _act_code(act) -> int:
+    return ACT[act] if isinstance(act, str) else int(act)
+
+
+def linear_act_fwd(x, w, b, act, y, z=None, stream=None) -> None:
+    """y = act(x w^T + b); z (optional) receives the pre-activation."""
+    ds = [desc(t) for t in (x, w, b)]
+    _check(lib.mt_linear_act_fwd(*[_ref(d) for d in ds], _act_code(act), _ref(desc(z)),
+                                 _ref(desc(y)), _stream(stream)), "mt_linear_act_fwd")
+
+
+def act_bwd_workspace(act, z, dy, dz, db=None) -> int:
+    n = _sz(0)
+    ds = [desc(t) for t in (z, dy, dz, db)]
+    _check(lib.mt_act_bwd_workspace(_act_code(act), *[_ref(d) for d in ds], ctypes.byref(n)),
+           "mt_act_bwd_workspace")
+    return int(n.value)
+
+
+def act_bwd(act, z, dy, dz, db=None, accumulate=False, workspace=None, stream=None) -> None:
+    """dz = dy * act'(z); db = column sums of dz (None skips it)."""
+    ds = [desc(t) for t in (z, dy, dz, db)]
+    ptr, nbytes = _ws(workspace)
+    _check(lib.mt_act_bwd(_act_code(act), *[_ref(d) for d in ds], ACCUMULATE if accumulate else 0,
+                          ptr, nbytes, _stream(stream)), "mt_act_bwd")
+
+
+def mse_loss_workspace(pred, target) -> int:
+    n = _sz(0)
+    _check(lib.mt_mse_loss_workspace(_ref(desc(pred)), _ref(desc(target)), ctypes.byref(n)),
+           "mt_mse_loss_workspace")
+    return int(n.value)
+
+
+def mse_loss(pred, target, loss=None, dpred=None, workspace=None, stream=None) -> None:
+    """loss = mean((pred - target)^2) (1-element tensor), dpred = 2 (pred - target) / N."""
+    ds = [desc(t) for t in (pred, target, loss, dpred)]
+    ptr, nbytes = _ws(workspace)
+    _check(lib.mt_mse_loss(*[_ref(d) for d in ds], ptr, nbytes, _stream(stream)), "mt_mse_loss")
+
+
+def _desc_array(ts):
+    arr = (MtTensor * max(1, len(ts)))()
+    for i, t in enumerate(ts):
+        arr[i] = desc(t)
+    return arr
+
+
+def sgd_step(params, grads, velocity, lr, momentum=0.0, weight_decay=0.0, stream=None) -> None:
+    """In place: v = momentum v + g + weight_decay p; p -= lr v (lists of tensors)."""
+    n = len(params)
+    assert len(grads) == n and len(velocity) == n
+    _check(lib.mt_sgd_step(n, _desc_array(params), _desc_array(grads), _desc_array(velocity),
+                           lr, momentum, weight_decay, _stream(stream)), "mt_sgd_step")
+
+
+def adam_step(params, grads, exp_avg, exp_avg_sq, lr, beta1, beta2, eps, step,
+              stream=None) -> None:
+    """In place Adam update at step `step` (>= 1) with bias-corrected moments."""
+    n = len(params)
+    assert len(grads) == n and len(exp_avg) == n and len(exp_avg_sq) == n
+    _check(lib.mt_adam_step(n, _desc_array(params), _desc_array(grads), _desc_array(exp_avg),
+                            _desc_array(exp_avg_sq), lr, beta1, beta2, eps, int(step),
+                            _stream(stream)), "mt_adam_step")
+
+
+def rmsprop_step(params, grads, sq_avg, lr, alpha, eps, stream=None) -> None:
+    """In place: v = alpha v + (1 - alpha) g^2; p -= lr g / sqrt(v + eps)."""
+    n = len(params)
+    assert len(grads) == n and len(sq_avg) == n
+    _check(lib.mt_rmsprop_step(n, _desc_array(params), _desc_array(grads), _desc_array(sq_avg),
+                               lr, alpha, eps, _stream(stream)), "mt_rmsprop_step")
 
 
 def _shape_call(fn, a, b, where):

@@ -2,14 +2,17 @@
 // dispatch. Declarations and their contracts: include/minitensor_hip.h.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <cmath>
 #include <cstdint>
 #include <cstdlib>
-#include <algorithm>
 #include <cstring>
 #include <string>
+#include <vector>
 
 #include "../../include/minitensor_hip.h"
 #include "gemm_params.hpp"
+#include "act.hpp"
 #include "kernels.hpp"
 #include "shape.hpp"
 
@@ -120,6 +123,21 @@ int choose_splits(int64_t blocks, int64_t stages) {
   s = std::min<int64_t>(s, stages / 8);
   s = std::min<int64_t>(s, 16);
   return s < 1 ? 1 : (int)s;
+}
+
+// Tiles that carry the dense-layer-with-nonlinearity epilogue: the 256x256
+// DMA tile for large products, else 128x128 or 64x64 (a forced cfg outside
+// these maps to the nearest of them).
+int choose_epi_cfg(int64_t M, int64_t N, bool vec) {
+  auto tiles = [&](int64_t bm, int64_t bn) { return cdiv(M, bm) * cdiv(N, bn); };
+  if (g_force_cfg >= 0) {
+    if (g_force_cfg == mt::kCfgDma256x256 && vec) return g_force_cfg;
+    if (g_force_cfg == mt::kCfg64x64) return g_force_cfg;
+    return mt::kCfg128x128;
+  }
+  if (vec && tiles(256, 256) >= 256) return mt::kCfgDma256x256;
+  if (tiles(128, 128) >= 128) return mt::kCfg128x128;
+  return mt::kCfg64x64;
 }
 
 void init_params(mt::GemmParams* p) {
@@ -493,13 +511,9 @@ mt_status reduce_impl(const mt_tensor* go, const mt_tensor* gi, uint32_t flags, 
                                        (flags & MT_ACCUMULATE) != 0, wsp, wsp ? parts : 1, stream));
 }
 
-}  // namespace
-
-extern "C" {
-
-mt_status mt_linear_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* b,
-                        const mt_tensor* y, void* stream) {
-  try {
+mt_status linear_fwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor* b, int32_t act,
+                          const mt_tensor* z, const mt_tensor* y, hipStream_t stream) {
+  {
     mt_status s;
     if ((s = check_matrix(x, "x")) || (s = check_matrix(w, "w")) ||
         (s = check_out_matrix(y, "y")))
@@ -509,6 +523,13 @@ mt_status mt_linear_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
     if (w->shape[1] != K) return fail(MT_ERR_SHAPE, "w must be [N, K] with x [M, K]");
     if (y->shape[0] != M || y->shape[1] != N) return fail(MT_ERR_SHAPE, "y must be [M, N]");
     if (b && (s = check_vector(b, "b", N))) return s;
+    if (act < 0 || act >= mt::kNumAct) return fail(MT_ERR_INVALID, "unknown activation");
+    if (z) {
+      if ((s = check_out_matrix(z, "z"))) return s;
+      if (z->shape[0] != M || z->shape[1] != N) return fail(MT_ERR_SHAPE, "z must be [M, N]");
+      if (overlaps(z, x) || overlaps(z, w) || overlaps(z, b) || overlaps(z, y))
+        return fail(MT_ERR_ALIAS, "z overlaps an input or y");
+    }
     const bool bf = x->dtype == MT_BF16;
     const int per = vec_elems(bf);
     if (overlaps(y, x) || overlaps(y, w) || overlaps(y, b))
@@ -531,9 +552,281 @@ mt_status mt_linear_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
     g.bf16 = bf;
     g.vec = vec_ok_operand(x->data, M, K, g.p.lda, nullptr, 0, per) &&
             vec_ok_operand(w->data, N, K, g.p.ldb, nullptr, 0, per) && aligned16(y->data) &&
-            N % 4 == 0 && g.p.ldc % 4 == 0 && (!g.p.bias || aligned16(g.p.bias));
+            N % 4 == 0 && g.p.ldc % 4 == 0 && (!g.p.bias || aligned16(g.p.bias)) &&
+            (!z || (aligned16(z->data) && pitch(z) % 4 == 0));
     g.cfg = -1;
-    return launch_gemm(g, (hipStream_t)stream, nullptr, 0);
+    if (act != mt::kActNone || z) {
+      g.p.act = act;
+      g.p.z = z ? (float*)z->data : nullptr;
+      g.p.ldz = z ? pitch(z) : 0;
+      g.cfg = choose_epi_cfg(M, N, g.vec);
+    }
+    return launch_gemm(g, stream, nullptr, 0);
+  }
+}
+
+
+
+// ------------------------------------------------------------- act_bwd
+mt_status act_bwd_impl(int32_t act, const mt_tensor* z, const mt_tensor* dy, const mt_tensor* dz,
+                       const mt_tensor* db, uint32_t flags, void* ws, size_t ws_bytes,
+                       hipStream_t stream, size_t* ws_query) {
+  if (flags & ~MT_ACCUMULATE) return fail(MT_ERR_INVALID, "mt_act_bwd: unknown flags");
+  if (act < 0 || act >= mt::kNumAct) return fail(MT_ERR_INVALID, "unknown activation");
+  mt_status s;
+  if ((s = check_matrix(z, "z")) || (s = check_matrix(dy, "dy")) || (s = check_matrix(dz, "dz")))
+    return s;
+  if (z->dtype != MT_F32) return fail(MT_ERR_DTYPE, "z (the saved pre-activation) must be f32");
+  if (dz->dtype != dy->dtype) return fail(MT_ERR_DTYPE, "dz must have dy's dtype");
+  const int64_t M = z->shape[0], N = z->shape[1];
+  if (dy->shape[0] != M || dy->shape[1] != N || dz->shape[0] != M || dz->shape[1] != N)
+    return fail(MT_ERR_SHAPE, "z, dy and dz must share one [M, N] shape");
+  if (dz->shape[0] > 1 && dz->stride[0] < dz->shape[1])
+    return fail(MT_ERR_LAYOUT, "dz: rows overlap (row pitch < columns)");
+  if (db && (s = check_vector(db, "db", N))) return s;
+  if (overlaps(dz, z) || overlaps(dz, dy) || overlaps(db, z) || overlaps(db, dy) ||
+      overlaps(db, dz))
+    return fail(MT_ERR_ALIAS, "an output overlaps an input or the other output");
+  int parts = 1;
+  if (db && M > 0 && N > 0) parts = g_force_parts > 0 ? g_force_parts : mt::colsum_parts(M, N);
+  const size_t need = parts > 1 ? (size_t)parts * N * sizeof(float) : 0;
+  if (ws_query) {
+    *ws_query = need;
+    return MT_OK;
+  }
+  if (ws && ((uintptr_t)ws & 255)) return fail(MT_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  float* wsp = (ws && need && ws_bytes >= need) ? (float*)ws : nullptr;
+  const bool acc = (flags & MT_ACCUMULATE) != 0;
+  (void)hipGetLastError();
+  return hip_status(mt::act_bwd(act, (const float*)z->data, pitch(z), dy->data, pitch(dy),
+                                dz->data, pitch(dz), dy->dtype == MT_BF16, M, N, acc,
+                                db ? (float*)db->data : nullptr, acc, wsp, wsp ? parts : 1,
+                                stream));
+}
+
+// ----------------------------------------------------------------- mse
+mt_status check_dense_f32(const mt_tensor* t, const char* name) {
+  mt_status s = check_tensor(t, name, 0, MT_MAX_DIMS);
+  if (s) return s;
+  if (t->dtype != MT_F32) return fail(MT_ERR_DTYPE, std::string(name) + ": must be f32");
+  if (!is_row_major(t)) return fail(MT_ERR_LAYOUT, std::string(name) + ": must be contiguous");
+  return MT_OK;
+}
+
+bool same_shape(const mt_tensor* a, const mt_tensor* b) {
+  if (a->ndim != b->ndim) return false;
+  for (int i = 0; i < a->ndim; ++i)
+    if (a->shape[i] != b->shape[i]) return false;
+  return true;
+}
+
+mt_status mse_impl(const mt_tensor* pred, const mt_tensor* target, const mt_tensor* loss,
+                   const mt_tensor* dpred, void* ws, size_t ws_bytes, hipStream_t stream,
+                   size_t* ws_query) {
+  mt_status s;
+  if ((s = check_dense_f32(pred, "pred")) || (s = check_dense_f32(target, "target"))) return s;
+  if (!same_shape(pred, target)) return fail(MT_ERR_SHAPE, "pred and target shapes differ");
+  const int64_t n = numel(pred);
+  const int parts = mt::mse_parts(n);
+  const size_t need = parts > 1 ? (size_t)parts * sizeof(float) : 0;
+  if (ws_query) {
+    *ws_query = need;
+    return MT_OK;
+  }
+  if (!loss && !dpred) return fail(MT_ERR_NULL, "mt_mse_loss: neither loss nor dpred given");
+  if (loss) {
+    if ((s = check_dense_f32(loss, "loss"))) return s;
+    if (numel(loss) != 1) return fail(MT_ERR_SHAPE, "loss must hold exactly one element");
+  }
+  if (dpred) {
+    if ((s = check_dense_f32(dpred, "dpred"))) return s;
+    if (!same_shape(dpred, pred)) return fail(MT_ERR_SHAPE, "dpred must have pred's shape");
+  }
+  if (overlaps(loss, pred) || overlaps(loss, target) || overlaps(dpred, pred) ||
+      overlaps(dpred, target) || overlaps(loss, dpred))
+    return fail(MT_ERR_ALIAS, "an output overlaps an input or the other output");
+  if (ws && ((uintptr_t)ws & 255)) return fail(MT_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  float* wsp = (ws && need && ws_bytes >= need) ? (float*)ws : nullptr;
+  (void)hipGetLastError();
+  return hip_status(mt::mse((const float*)pred->data, (const float*)target->data, n,
+                            dpred ? (float*)dpred->data : nullptr,
+                            loss ? (float*)loss->data : nullptr, wsp, wsp ? parts : 1, stream));
+}
+
+// ---------------------------------------------------------- optimizers
+// Validates n (param, grad, state...) tuples of contiguous f32 tensors of one
+// shape each, with no output overlapping anything else, and packs them into
+// launches of up to kOptMaxTensors tensors.
+mt_status plan_opt(int32_t n, const mt_tensor* params, const mt_tensor* grads,
+                   const mt_tensor* st1, const mt_tensor* st2, const char* who,
+                   std::vector<mt::OptBatch>* out) {
+  if (n < 0) return fail(MT_ERR_INVALID, std::string(who) + ": negative tensor count");
+  if (n > 0 && (!params || !grads || !st1)) return fail(MT_ERR_NULL, std::string(who) + ": null array");
+  const std::string w(who);
+  std::vector<const mt_tensor*> outs;  // every tensor written
+  for (int32_t i = 0; i < n; ++i) {
+    const mt_tensor* ts[4] = {&params[i], &grads[i], &st1[i], st2 ? &st2[i] : nullptr};
+    const char* names[4] = {"param", "grad", "state", "state2"};
+    for (int j = 0; j < 4; ++j) {
+      if (!ts[j]) continue;
+      mt_status s = check_dense_f32(ts[j], (w + ": " + names[j] + " " + std::to_string(i)).c_str());
+      if (s) return s;
+      if (!same_shape(ts[j], ts[0]))
+        return fail(MT_ERR_SHAPE, w + ": tensor " + std::to_string(i) + " has mismatched shapes");
+    }
+    outs.push_back(ts[0]);
+    outs.push_back(ts[2]);
+    if (ts[3]) outs.push_back(ts[3]);
+  }
+  // outputs overlap no output and no gradient
+  for (size_t a = 0; a < outs.size(); ++a) {
+    for (size_t b = a + 1; b < outs.size(); ++b)
+      if (overlaps(outs[a], outs[b])) return fail(MT_ERR_ALIAS, w + ": updated tensors overlap");
+    for (int32_t i = 0; i < n; ++i)
+      if (overlaps(outs[a], &grads[i]))
+        return fail(MT_ERR_ALIAS, w + ": an updated tensor overlaps a gradient");
+  }
+  mt::OptBatch cur{};
+  for (int32_t i = 0; i < n; ++i) {
+    const int64_t cnt = numel(&params[i]);
+    if (cnt == 0) continue;
+    if (cur.n == mt::kOptMaxTensors) {
+      out->push_back(cur);
+      cur = mt::OptBatch{};
+    }
+    const int k = cur.n++;
+    cur.param[k] = (float*)params[i].data;
+    cur.grad[k] = (const float*)grads[i].data;
+    cur.state1[k] = (float*)st1[i].data;
+    cur.state2[k] = st2 ? (float*)st2[i].data : nullptr;
+    cur.numel[k] = cnt;
+    cur.vec[k] = aligned16(params[i].data) && aligned16(grads[i].data) && aligned16(st1[i].data) &&
+                 (!st2 || aligned16(st2[i].data));
+  }
+  if (cur.n > 0) out->push_back(cur);
+  return MT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+mt_status mt_linear_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* b,
+                        const mt_tensor* y, void* stream) {
+  try {
+    return linear_fwd_impl(x, w, b, mt::kActNone, nullptr, y, (hipStream_t)stream);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_linear_act_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* b,
+                            int32_t act, const mt_tensor* z, const mt_tensor* y, void* stream) {
+  try {
+    return linear_fwd_impl(x, w, b, act, z, y, (hipStream_t)stream);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_act_bwd(int32_t act, const mt_tensor* z, const mt_tensor* dy, const mt_tensor* dz,
+                     const mt_tensor* db, uint32_t flags, void* ws, size_t ws_bytes,
+                     void* stream) {
+  try {
+    return act_bwd_impl(act, z, dy, dz, db, flags, ws, ws_bytes, (hipStream_t)stream, nullptr);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_act_bwd_workspace(int32_t act, const mt_tensor* z, const mt_tensor* dy,
+                               const mt_tensor* dz, const mt_tensor* db, size_t* bytes) {
+  try {
+    if (!bytes) return fail(MT_ERR_NULL, "bytes is null");
+    return act_bwd_impl(act, z, dy, dz, db, 0, nullptr, 0, nullptr, bytes);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_mse_loss(const mt_tensor* pred, const mt_tensor* target, const mt_tensor* loss,
+                      const mt_tensor* dpred, void* ws, size_t ws_bytes, void* stream) {
+  try {
+    return mse_impl(pred, target, loss, dpred, ws, ws_bytes, (hipStream_t)stream, nullptr);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_mse_loss_workspace(const mt_tensor* pred, const mt_tensor* target, size_t* bytes) {
+  try {
+    if (!bytes) return fail(MT_ERR_NULL, "bytes is null");
+    return mse_impl(pred, target, nullptr, nullptr, nullptr, 0, nullptr, bytes);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_sgd_step(int32_t n, const mt_tensor* params, const mt_tensor* grads,
+                      const mt_tensor* velocity, float lr, float momentum, float weight_decay,
+                      void* stream) {
+  try {
+    if (!std::isfinite(lr) || !std::isfinite(momentum) || !std::isfinite(weight_decay))
+      return fail(MT_ERR_INVALID, "mt_sgd_step: lr, momentum and weight_decay must be finite");
+    std::vector<mt::OptBatch> batches;
+    mt_status s = plan_opt(n, params, grads, velocity, nullptr, "mt_sgd_step", &batches);
+    if (s) return s;
+    (void)hipGetLastError();
+    for (const auto& b : batches)
+      if ((s = hip_status(mt::sgd_step(b, lr, momentum, weight_decay, (hipStream_t)stream))))
+        return s;
+    return MT_OK;
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_adam_step(int32_t n, const mt_tensor* params, const mt_tensor* grads,
+                       const mt_tensor* exp_avg, const mt_tensor* exp_avg_sq, float lr, float beta1,
+                       float beta2, float eps, int64_t step, void* stream) {
+  try {
+    if (!std::isfinite(lr) || !(beta1 >= 0.f && beta1 < 1.f) || !(beta2 >= 0.f && beta2 < 1.f) ||
+        !(eps >= 0.f) || !std::isfinite(eps))
+      return fail(MT_ERR_INVALID, "mt_adam_step: needs finite lr, 0 <= beta < 1, finite eps >= 0");
+    if (step < 1) return fail(MT_ERR_INVALID, "mt_adam_step: step counts from 1");
+    std::vector<mt::OptBatch> batches;
+    mt_status s = plan_opt(n, params, grads, exp_avg, exp_avg_sq, "mt_adam_step", &batches);
+    if (s) return s;
+    // bias corrections 1 / (1 - beta^t) in double, then rounded once
+    const double bc1 = 1.0 - std::pow((double)beta1, (double)step);
+    const double bc2 = 1.0 - std::pow((double)beta2, (double)step);
+    const float inv_bc1 = (float)(1.0 / bc1), inv_bc2 = (float)(1.0 / bc2);
+    if (!std::isfinite(inv_bc1) || !std::isfinite(inv_bc2))
+      return fail(MT_ERR_INVALID, "mt_adam_step: bias correction 1 - beta^step underflows to 0");
+    (void)hipGetLastError();
+    for (const auto& b : batches)
+      if ((s = hip_status(mt::adam_step(b, lr, beta1, beta2, eps, inv_bc1, inv_bc2,
+                                        (hipStream_t)stream))))
+        return s;
+    return MT_OK;
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_rmsprop_step(int32_t n, const mt_tensor* params, const mt_tensor* grads,
+                          const mt_tensor* sq_avg, float lr, float alpha, float eps, void* stream) {
+  try {
+    if (!std::isfinite(lr) || !(alpha >= 0.f && alpha <= 1.f) || !(eps >= 0.f) ||
+        !std::isfinite(eps))
+      return fail(MT_ERR_INVALID, "mt_rmsprop_step: needs finite lr, 0 <= alpha <= 1, finite eps >= 0");
+    std::vector<mt::OptBatch> batches;
+    mt_status s = plan_opt(n, params, grads, sq_avg, nullptr, "mt_rmsprop_step", &batches);
+    if (s) return s;
+    (void)hipGetLastError();
+    for (const auto& b : batches)
+      if ((s = hip_status(mt::rmsprop_step(b, lr, alpha, eps, (hipStream_t)stream)))) return s;
+    return MT_OK;
   } catch (...) {
     return fail(MT_ERR_INVALID, "internal error");
   }

@@ -7,7 +7,8 @@
 
 namespace mt {
 
-template <bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int WGN, int VEC, int WPE>
+template <bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int WGN, int VEC, int WPE,
+          bool EPI = false>
 static hipError_t launch_bf16(const GemmParams& p, hipStream_t stream) {
   GemmParams q = p;
   q.tiles_m = (int32_t)((p.M + BM - 1) / BM);
@@ -15,12 +16,13 @@ static hipError_t launch_bf16(const GemmParams& p, hipStream_t stream) {
   const int64_t blocks = (int64_t)q.tiles_m * q.tiles_n * p.keep_count * p.splits;
   if (blocks <= 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((gemm::gemm_kernel<__bf16, A_KC, B_KC, BM, BN, BK, WGM, WGN, VEC, WPE>),
+  hipLaunchKernelGGL((gemm::gemm_kernel<__bf16, A_KC, B_KC, BM, BN, BK, WGM, WGN, VEC, WPE, EPI>),
                      dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
   return hipGetLastError();
 }
 
-template <bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int WGN, int NS, int WPE>
+template <bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int WGN, int NS, int WPE,
+          bool EPI = false>
 static hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
   GemmParams q = p;
   q.tiles_m = (int32_t)((p.M + BM - 1) / BM);
@@ -30,10 +32,10 @@ static hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   // the per-load K-tail test only where K is not a whole number of stages
   if (p.K % BK != 0)
-    hipLaunchKernelGGL((gemm::gemm_dma_kernel<__bf16, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 1, 1, true, WPE>),
+    hipLaunchKernelGGL((gemm::gemm_dma_kernel<__bf16, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 1, 1, true, WPE, EPI>),
                        dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
   else
-    hipLaunchKernelGGL((gemm::gemm_dma_kernel<__bf16, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 1, 1, false, WPE>),
+    hipLaunchKernelGGL((gemm::gemm_dma_kernel<__bf16, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 1, 1, false, WPE, EPI>),
                        dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
   return hipGetLastError();
 }
@@ -60,8 +62,25 @@ static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream
   }
 }
 
+// The dense layer followed by a nonlinearity (z / act set): the forward
+// layout only, on the 256x256 DMA tile or the 128x128 / 64x64 tiles.
+static hipError_t launch_epi(const GemmParams& p, bool vec, int cfg, hipStream_t stream) {
+  if (vec) {
+    if (cfg == kCfgDma256x256)
+      return launch_dma<true, true, 256, 256, 64, 2, 4, 2, 2, true>(p, stream);
+    if (cfg == kCfg128x128) return launch_bf16<true, true, 128, 128, 32, 2, 2, 8, 2, true>(p, stream);
+    return launch_bf16<true, true, 64, 64, 32, 2, 2, 8, 4, true>(p, stream);
+  }
+  if (cfg == kCfg128x128) return launch_bf16<true, true, 128, 128, 32, 2, 2, 1, 2, true>(p, stream);
+  return launch_bf16<true, true, 64, 64, 32, 2, 2, 1, 4, true>(p, stream);
+}
+
 hipError_t gemm_bf16(const GemmParams& p, bool a_kc, bool b_kc, bool vec, int cfg,
                      hipStream_t stream) {
+  if (p.act || p.z) {
+    if (!a_kc || !b_kc) return hipErrorInvalidValue;
+    return launch_epi(p, vec, cfg, stream);
+  }
   if (vec) {
     if (a_kc && b_kc) return launch_layout<true, true, 8>(p, cfg, stream);
     if (a_kc && !b_kc) return launch_layout<true, false, 8>(p, cfg, stream);

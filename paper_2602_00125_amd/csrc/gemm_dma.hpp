@@ -277,7 +277,7 @@ struct DmaMma<__bf16, A_KC, B_KC, TM, TN, BK, BM, BN> {
 
 template <typename T, bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int WGN, int NS,
           int DMA_G0, int DMA_GS, bool KTAIL,
-          int WAVES_PER_EU>
+          int WAVES_PER_EU, bool EPI = false>
 __global__ __launch_bounds__(WGM * WGN * 64)
 __attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
 void gemm_dma_kernel(const GemmParams p) {
@@ -466,6 +466,10 @@ void gemm_dma_kernel(const GemmParams p) {
   wait_vmcnt<0>();
 
   // ---- epilogue (as in gemm_kernel): lane holds C[m][n0' + 8g + 4h + 0..3]
+  if constexpr (EPI) {
+    act_epilogue<TM, TN, true>(p, acc, m0 + wm * WTM + l32, n0 + wn * WTN + 4 * h);
+    return;
+  }
   const bool to_partial = p.splits > 1;
   float* C = to_partial ? p.partial + (int64_t)split * p.partial_stride + batch * p.M * p.N
                         : p.c + c_off;

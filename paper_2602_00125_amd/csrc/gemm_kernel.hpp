@@ -33,6 +33,7 @@
 #pragma once
 #include <hip/hip_runtime.h>
 
+#include "act.hpp"
 #include "gemm_params.hpp"
 
 namespace mt {
@@ -248,8 +249,66 @@ struct Mma<__bf16, A_KC, B_KC, TM, TN, BK, PA, PB> {
 template <typename T> struct LdsElem { using type = T; };
 template <> struct LdsElem<__bf16> { using type = unsigned short; };
 
+// Epilogue of the dense layer followed by a nonlinearity (Sec. 3.3 Eq. (5),
+// "Nonlinearities"): z = acc + b[n] is stored when p.z is set and act(z) goes
+// to C. No batch, split or accumulation (the host guarantees it). The lane
+// holds C[m0l + 32 i][n0l + 32 q + 8 g + 0..3] in acc[i][q][4g .. 4g+3]. One
+// copy per nonlinearity: the switch is taken once per block, outside the
+// unrolled stores.
+template <int ACT, int TM, int TN, bool VEC_C>
+__device__ __forceinline__ void act_store(const GemmParams& p, const f32x16 (&acc)[TM][TN],
+                                          int64_t m0l, int64_t n0l) {
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int64_t m = m0l + i * 32;
+    if (m >= p.M) continue;
+    float* crow = p.c + m * p.ldc;
+    float* zrow = p.z ? p.z + m * p.ldz : nullptr;
+#pragma unroll
+    for (int q = 0; q < TN; ++q) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int64_t n = n0l + q * 32 + 8 * g;
+        f32x4 v = {acc[i][q][4 * g + 0], acc[i][q][4 * g + 1], acc[i][q][4 * g + 2],
+                   acc[i][q][4 * g + 3]};
+        if (VEC_C) {
+          if (n >= p.N) continue;
+          if (p.bias) v += *(const f32x4*)&p.bias[n];
+          if (zrow) *(f32x4*)&zrow[n] = v;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = act_apply_t<ACT>(v[e]);
+          *(f32x4*)&crow[n] = v;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (n + e >= p.N) continue;
+            float x = v[e];
+            if (p.bias) x += p.bias[n + e];
+            if (zrow) zrow[n + e] = x;
+            crow[n + e] = act_apply_t<ACT>(x);
+          }
+        }
+      }
+    }
+  }
+}
+
+template <int TM, int TN, bool VEC_C>
+__device__ __forceinline__ void act_epilogue(const GemmParams& p, const f32x16 (&acc)[TM][TN],
+                                             int64_t m0l, int64_t n0l) {
+  switch (p.act) {
+    case kActRelu: act_store<kActRelu, TM, TN, VEC_C>(p, acc, m0l, n0l); break;
+    case kActSigmoid: act_store<kActSigmoid, TM, TN, VEC_C>(p, acc, m0l, n0l); break;
+    case kActTanh: act_store<kActTanh, TM, TN, VEC_C>(p, acc, m0l, n0l); break;
+    case kActGelu: act_store<kActGelu, TM, TN, VEC_C>(p, acc, m0l, n0l); break;
+    default: act_store<kActNone, TM, TN, VEC_C>(p, acc, m0l, n0l); break;
+  }
+}
+
+// EPI: the dense-layer-with-nonlinearity epilogue (act_epilogue) instead of
+// the plain one; instantiated only for the forward layout and a few tiles.
 template <typename T, bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int WGN, int VEC,
-          int WAVES_PER_EU>
+          int WAVES_PER_EU, bool EPI = false>
 __global__ __launch_bounds__(WGM * WGN * 64)
 __attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
 void gemm_kernel(const GemmParams p) {
@@ -376,6 +435,10 @@ void gemm_kernel(const GemmParams p) {
   }
 
   // ---- epilogue: lane holds C[m][n0' + 8g + 4h + 0..3] in acc regs 4g..4g+3
+  if constexpr (EPI) {
+    act_epilogue<TM, TN, (VEC > 1)>(p, acc, m0 + wm * WTM + l32, n0 + wn * WTN + 4 * h);
+    return;
+  }
   const bool to_partial = p.splits > 1;
   float* C = to_partial ? p.partial + (int64_t)split * p.partial_stride + batch * p.M * p.N
                         : p.c + c_off;

@@ -44,6 +44,12 @@ struct GemmParams {
   int64_t stages_per_split;
   float* partial;
   int64_t partial_stride;
+  // epilogue of the dense layer followed by a nonlinearity (no batch, no
+  // split, no accumulation): z (nullable, row pitch ldz) receives the biased
+  // product, C receives act(that) (act: an ActKind, 0 = none)
+  float* z;
+  int64_t ldz;
+  int32_t act;
 };
 
 }  // namespace mt

@@ -64,4 +64,43 @@ int reduce_parts(const ReducePlan& plan);
 // out[i] = value (i < n), a small fill kernel (used instead of hipMemsetAsync).
 hipError_t fill_f32(float* out, int64_t n, float value, hipStream_t stream);
 
+// out[n] (+)= sum_p ws[p][n] over p = 0 .. parts-1 in order (second pass of
+// the row-sliced column sums).
+hipError_t parts_finish(const float* ws, int parts, int64_t N, float* out, bool accumulate,
+                        hipStream_t stream);
+
+// Pullback of H = act(Z) for row-major [M][N] matrices with row pitches:
+// dz (+)= dh * act'(z) (dh and dz f32, or both bf16: dz rounded to nearest
+// even), and, when db is given, db[n] (+)= sum_m dh * act'(z) of the fp32
+// terms. ws: room for `parts` x N floats (row slices, fixed-order second
+// pass); parts = 1 needs none.
+hipError_t act_bwd(int act, const float* z, int64_t ldz, const void* dh, int64_t ldh, void* dz,
+                   int64_t ldd, bool is_bf16, int64_t M, int64_t N, bool acc_dz, float* db,
+                   bool acc_db, float* ws, int parts, hipStream_t stream);
+
+// Mean squared error over n contiguous fp32 elements: *loss = sum (p - t)^2 / n
+// (nullable), dp = 2 (p - t) / n (nullable). ws: room for `parts` floats
+// (block partials added in order by a second pass); parts = 1 needs none.
+hipError_t mse(const float* p, const float* t, int64_t n, float* dp, float* loss, float* ws,
+               int parts, hipStream_t stream);
+int mse_parts(int64_t n);
+
+// Up to kOptMaxTensors contiguous fp32 parameter tensors updated in one launch.
+constexpr int kOptMaxTensors = 32;
+struct OptBatch {
+  int32_t n;
+  float* param[kOptMaxTensors];
+  const float* grad[kOptMaxTensors];
+  float* state1[kOptMaxTensors];  // SGD velocity, Adam first moment, RMSprop average
+  float* state2[kOptMaxTensors];  // Adam second moment
+  int64_t numel[kOptMaxTensors];
+  int64_t block_start[kOptMaxTensors + 1];  // filled by the launcher
+  int8_t vec[kOptMaxTensors];               // every pointer of the tensor 16-byte aligned
+};
+hipError_t sgd_step(const OptBatch& b, float lr, float momentum, float weight_decay,
+                    hipStream_t stream);
+hipError_t adam_step(const OptBatch& b, float lr, float beta1, float beta2, float eps,
+                     float inv_bc1, float inv_bc2, hipStream_t stream);
+hipError_t rmsprop_step(const OptBatch& b, float lr, float alpha, float eps, hipStream_t stream);
+
 }  // namespace mt

@@ -280,6 +280,14 @@ hipError_t splitk_finish(const float* partial, int splits, int64_t M, int64_t N,
   return hipGetLastError();
 }
 
+hipError_t parts_finish(const float* ws, int parts, int64_t N, float* out, bool accumulate,
+                        hipStream_t stream) {
+  if (N <= 0) return hipSuccess;
+  hipLaunchKernelGGL(parts_finish_kernel, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, stream,
+                     ws, parts, N, out, (int)accumulate);
+  return hipGetLastError();
+}
+
 hipError_t fill_f32(float* out, int64_t n, float value, hipStream_t stream) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(fill_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, out, n,
