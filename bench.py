@@ -194,6 +194,127 @@ def bench_bmm(args, w, inp, dev):
     print(json.dumps(out), flush=True)
 
 
+def cpu_baseline_mlp(inp, seconds: float):
+    """Time the fp64 oracle on sampled rows of the perceptron's forward pass:
+    each sampled row goes through both dense layers, the nonlinearity and the
+    loss gradient, as the oracle computes them."""
+    import numpy as np
+
+    import oracle
+    from oracle import nn as onn
+
+    X, W1, b1, W2, b2, T = (inp[k].double().numpy() for k in ("X", "W1", "b1", "W2", "b2", "T"))
+    M = X.shape[0]
+    rng = np.random.default_rng(0)
+    macs = rows = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        idx = rng.integers(0, M, 16)   # 16 rows: the oracle runs one thread per row
+        Z, H, _ = onn.linear_act_fwd(X[idx], W1, b1, onn.GELU)
+        P, _ = oracle.linear_fwd(H, W2, b2)
+        onn.mse_loss(P, T[idx])
+        macs += len(idx) * (W1.size + W2.size)
+        rows += len(idx)
+    el = time.perf_counter() - t0
+    return {"value": 2.0 * macs / el / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"{rows} random rows of X through both dense layers, GELU and the MSE "
+                      f"gradient in fp64 (with the |a*b| bound) in {el:.1f} s; TFLOP/s = 2*MACs/s"}
+
+
+def bench_mlp(args, w, inp, dev):
+    """Two-layer perceptron training step: forward with the fused GELU
+    epilogue, MSE, backward (dH1, dW2, db2, the GELU pullback with db1 folded
+    in, dW1), and one Adam update of all four parameters."""
+    import torch
+
+    from paper_2602_00125_amd import binding as mt
+
+    x, W1, b1, W2, b2, t = (inp[k].to(dev) for k in ("X", "W1", "b1", "W2", "b2", "T"))
+    M, D1, D2 = w.M, w.D1, w.D2
+    z1 = torch.empty(M, D1, device=dev)
+    h1 = torch.empty(M, D1, device=dev)
+    pr = torch.empty(M, D2, device=dev)
+    loss = torch.empty(1, device=dev)
+    dp = torch.empty(M, D2, device=dev)
+    dh1 = torch.empty(M, D1, device=dev)
+    dz1 = torch.empty(M, D1, device=dev)
+    params = [W1, b1, W2, b2]
+    grads = [torch.empty_like(p) for p in params]
+    ms = [torch.zeros_like(p) for p in params]
+    vs = [torch.zeros_like(p) for p in params]
+    need = max(mt.linear_bwd_workspace(h1, W2, dp, dh1, grads[2], grads[3]),
+               mt.act_bwd_workspace(w.act, z1, dh1, dz1, grads[1]),
+               mt.linear_bwd_workspace(x, W1, dz1, None, grads[0], None),
+               mt.mse_loss_workspace(pr, t))
+    ws = torch.empty(need // 4 + 64, device=dev) if need else None
+    counter = [0]
+
+    def step(ev=None):
+        counter[0] += 1
+        marks = iter(ev) if ev is not None else None
+
+        def mark():
+            if marks is not None:
+                next(marks).record()
+        mark()
+        mt.linear_act_fwd(x, W1, b1, w.act, h1, z=z1)
+        mark()
+        mt.linear_fwd(h1, W2, b2, pr)
+        mark()
+        mt.mse_loss(pr, t, loss, dp, workspace=ws)
+        mark()
+        if ev is None:
+            mt.linear_bwd(h1, W2, dp, dh1, grads[2], grads[3], workspace=ws)
+        else:
+            mt.linear_bwd(h1, W2, dp, dh1, None, None, workspace=ws)
+            mark()
+            mt.linear_bwd(h1, W2, dp, None, grads[2], None, workspace=ws)
+            mark()
+            mt.linear_bwd(h1, W2, dp, None, None, grads[3], workspace=ws)
+        mark()
+        mt.act_bwd(w.act, z1, dh1, dz1, grads[1], workspace=ws)
+        mark()
+        mt.linear_bwd(x, W1, dz1, None, grads[0], None, workspace=ws)
+        mark()
+        mt.adam_step(params, grads, ms, vs, 1e-4, 0.9, 0.999, 1e-8, counter[0])
+        mark()
+
+    names = ["fwd1_nt_gemm_gelu", "fwd2_nt_gemm", "mse", "dh1_nn_gemm", "dw2_tn_gemm",
+             "db2_colsum", "act_bwd_db1", "dw1_tn_gemm", "adam"]
+    ms_step, _ = timed_steps(step, 1, args.steps, args.warmup)
+    _, per = timed_steps(step, len(names) + 1, args.steps, 1)
+    per = dict(zip(names, per))
+    value = w.flops() / (ms_step * 1e-3) / 1e12
+    gemm_flops = {"fwd1_nt_gemm_gelu": 2.0 * M * w.D0 * D1, "fwd2_nt_gemm": 2.0 * M * D1 * D2,
+                  "dh1_nn_gemm": 2.0 * M * D2 * D1, "dw2_tn_gemm": 2.0 * M * D2 * D1,
+                  "dw1_tn_gemm": 2.0 * M * D1 * w.D0}
+    dominant = max(gemm_flops, key=lambda k: per[k])
+    achieved = gemm_flops[dominant] / (per[dominant] * 1e-3) / 1e12
+    nparam = sum(p.numel() for p in params)
+    hbm_bytes = {"act_bwd_db1": 12.0 * M * D1 + 4 * D1, "mse": 12.0 * M * D2 + 4,
+                 "adam": 28.0 * nparam, "db2_colsum": 4.0 * M * D2 + 4 * D2}
+    hbm = {k: {"ms": round(per[k], 4), "gbs": round(v / (per[k] * 1e-3) / 1e9, 1),
+               "frac": round(v / (per[k] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "bytes": int(v)}
+           for k, v in hbm_bytes.items()}
+    out = {"metric": f"TFLOP/s for a two-layer perceptron training step (5 GEMMs + GELU, MSE, "
+                     f"Adam) on {args.workload}",
+           "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": args.workload, "M": M, "D0": w.D0, "D1": D1, "D2": D2,
+                      "act": w.act, "optimizer": "adam",
+                      "pct_of_mfma_peak": round(100.0 * value / FP32_MFMA_PEAK_TFLOPS, 2)},
+           "roofline": {"bound": "mfma", "kernel": dominant, "achieved": round(achieved, 3),
+                        "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                        "frac": round(achieved / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": None},
+           "kernels_ms": {k: round(v, 4) for k, v in per.items()},
+           "hbm_kernels": hbm,
+           "loss_after_timed_steps": round(float(loss.item()), 6)}
+    out["cpu_baseline"] = cpu_baseline_mlp(inp, args.cpu_seconds) if args.cpu_seconds > 0 else None
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_probe:
@@ -213,6 +334,8 @@ def main():
     inp = w.make()
     if isinstance(w, wl.BmmWorkload):
         return bench_bmm(args, w, inp, dev)
+    if isinstance(w, wl.MlpWorkload):
+        return bench_mlp(args, w, inp, dev)
     x, wt, bias, dy = (inp[k].to(dev) for k in ("X", "W", "b", "dY"))
     M, N, K = w.M, w.N, w.K
     y = torch.empty(M, N, device=dev)

@@ -91,6 +91,35 @@ class BmmWorkload:
         return {n: _draw(g, shapes[n], self.dist.get(n, ("uniform", 1.0))) for n in ("A", "B", "dC")}
 
 
+@dataclass
+class MlpWorkload:
+    """A two-layer perceptron training step: P = Dense2(act(Dense1(X))), the
+    mean squared error against T, the backward pass and an Adam update of
+    W1, b1, W2, b2. X[M,D0], W1[D1,D0], b1[D1], W2[D2,D1], b2[D2], T[M,D2],
+    all fp32."""
+    name: str
+    M: int
+    D0: int
+    D1: int
+    D2: int
+    act: str = "gelu"
+    dist: dict = field(default_factory=dict)
+    seed: int = 0
+
+    def flops(self) -> float:
+        """Multiply-adds of the five products of a step (both forwards, dH1,
+        dW2, dW1; the input layer's dX is not needed), 2 flops each."""
+        return 2.0 * self.M * (2 * self.D0 * self.D1 + 3 * self.D1 * self.D2)
+
+    def make(self, seed: int | None = None) -> dict:
+        g = torch.Generator("cpu")
+        g.manual_seed(self.seed if seed is None else seed)
+        shapes = {"X": (self.M, self.D0), "W1": (self.D1, self.D0), "b1": (self.D1,),
+                  "W2": (self.D2, self.D1), "b2": (self.D2,), "T": (self.M, self.D2)}
+        return {n: _draw(g, shapes[n], self.dist.get(n, ("uniform", 1.0)))
+                for n in ("X", "W1", "b1", "W2", "b2", "T")}
+
+
 def _u(a):
     return ("uniform", a)
 
@@ -114,9 +143,16 @@ LINEAR_16384x8192x8192_BF16 = LinearWorkload(
     "linear_16384x8192x8192_bf16", M=16384, N=8192, K=8192, dtype="bf16",
     dist={"X": N01, "W": _u(1 / math.sqrt(8192)), "b": _u(1 / math.sqrt(8192)), "dY": N01})
 
+# The training step around the dense layer: 8192 rows through 8192 -> 8192
+# (GELU) -> 8192 under MSE with Adam; weights scaled like the dense layers above.
+MLP2_8192x8192x8192x8192_F32_GELU = MlpWorkload(
+    "mlp2_8192x8192x8192x8192_f32_gelu", M=8192, D0=8192, D1=8192, D2=8192, act="gelu",
+    dist={"X": N01, "W1": _u(1 / math.sqrt(8192)), "b1": _u(1 / math.sqrt(8192)),
+          "W2": _u(1 / math.sqrt(8192)), "b2": _u(1 / math.sqrt(8192)), "T": N01})
+
 WORKLOADS = {w.name: w for w in (LINEAR_64x32x128_F32, LINEAR_4096x1024x1024_F32,
                                  LINEAR_8192x8192x8192_F32, BMM_BCAST_16x1x509x257_1x8x257x383_F32,
-                                 LINEAR_16384x8192x8192_BF16)}
+                                 LINEAR_16384x8192x8192_BF16, MLP2_8192x8192x8192x8192_F32_GELU)}
 
 
 def linear(M, N, K, dtype="f32", dist=None, seed=0, name=None) -> LinearWorkload:

@@ -259,6 +259,12 @@ def test_mse_empty():
 SHAPES = [(1,), (7,), (4096,), (300, 257), (1024, 1024), (0,), (5, 3)]
 
 
+def f32(*xs):
+    """The fp32 values the C ABI receives for float hyperparameters; the
+    oracle takes the same numbers (e.g. 1 - beta is then exact on both sides)."""
+    return [float(np.float32(x)) for x in xs]
+
+
 def _tensors(seed, unaligned=False):
     out = []
     for i, s in enumerate(SHAPES):
@@ -275,7 +281,7 @@ def _tensors(seed, unaligned=False):
 @pytest.mark.parametrize("unaligned", [False, True])
 def test_sgd_steps(unaligned):
     ps, vs = _tensors(0, unaligned), [t.abs() * 0.1 for t in _tensors(50)]
-    lr, mu, wd = 0.05, 0.9, 1e-2
+    lr, mu, wd = f32(0.05, 0.9, 1e-2)
     for step in range(3):
         gs = _tensors(100 + step)
         before = [(to_f64(p), to_f64(g), to_f64(v)) for p, g, v in zip(ps, gs, vs)]
@@ -292,7 +298,7 @@ def test_adam_steps(unaligned):
     ps = _tensors(0, unaligned)
     ms = [torch.zeros_like(p) for p in ps]
     vs = [torch.zeros_like(p) for p in ps]
-    lr, b1, b2, eps = 1e-2, 0.9, 0.999, 1e-8
+    lr, b1, b2, eps = f32(1e-2, 0.9, 0.999, 1e-8)
     for t in range(1, 5):
         gs = _tensors(200 + t)
         before = [tuple(to_f64(x) for x in q) for q in zip(ps, gs, ms, vs)]
@@ -308,7 +314,7 @@ def test_adam_steps(unaligned):
 def test_rmsprop_steps():
     ps = _tensors(0)
     vs = [torch.zeros_like(p) for p in ps]
-    lr, alpha, eps = 1e-2, 0.99, 1e-8
+    lr, alpha, eps = f32(1e-2, 0.99, 1e-8)
     for step in range(3):
         gs = _tensors(300 + step)
         before = [tuple(to_f64(x) for x in q) for q in zip(ps, gs, vs)]
@@ -327,10 +333,11 @@ def test_optimizer_many_tensors_one_call():
     gs = [wl.tensor(s, ("normal",), seed=100 + i).to(DEV) for i, s in enumerate(shapes)]
     vs = [torch.zeros_like(p) for p in ps]
     before = [(to_f64(p), to_f64(g)) for p, g in zip(ps, gs)]
-    b.sgd_step(ps, gs, vs, 0.1, 0.0, 0.0)
+    lr = f32(0.1)[0]
+    b.sgd_step(ps, gs, vs, lr, 0.0, 0.0)
     torch.cuda.synchronize()
     for (p0, g0), p in zip(before, ps):
-        th, _, St, _ = onn.sgd_step(p0, g0, np.zeros_like(p0), 0.1, 0.0, 0.0)
+        th, _, St, _ = onn.sgd_step(p0, g0, np.zeros_like(p0), lr, 0.0, 0.0)
         assert_close(to_f64(p), th, 1e-6 * St + 1e-38, rel=1.0, abs_=0.0, what="param")
 
 
