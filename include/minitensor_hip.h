@@ -259,7 +259,9 @@ mt_status mt_matmul_shape(int32_t na, const int64_t* a, int32_t nb, const int64_
  * allow 16-byte loads run at 128x128 or 64x64 whatever is forced); "vec1"
  * (1 = force the narrow-load kernels); "splits" (0..4096, split-K count for
  * mt_linear_bwd's dw, 0 = automatic); "parts" (0..4096, row slices of the db
- * and broadcast-gradient reductions, 0 = automatic). Results stay within the
+ * and broadcast-gradient reductions, 0 = automatic); "krot" (1 = the default:
+ * blocks of the 256x256 DMA tile start their K loop at a stage that depends
+ * on their XCD and wrap around; 0 = every block starts at k = 0). Results stay within the
  * documented accuracy for every setting. */
 int mt_debug_set(const char* key, int64_t value);
 

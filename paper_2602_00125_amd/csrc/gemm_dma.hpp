@@ -370,6 +370,16 @@ void gemm_dma_kernel(const GemmParams p) {
     b_nxt = uniform_ptr(B + (rb_off + (B_KC ? n0 * p.ldb + k0 : k0 * p.ldb + n0)) * ES);
     k_left = uniform_i64(p.K - k0);
   };
+  // K-stage rotation (p.krot): the sequence starts at stage rot and wraps to
+  // stage 0 once, where the tile origins are sought again
+  bool wrap_pending = false;
+  if (p.krot && p.splits == 1 && p.red_count == 1 && KS > 1) {
+    const int64_t rot = ((int64_t)(blockIdx.x & 7) * KS) >> 3;
+    if (rot > 0) {
+      cur_kt = uniform_i64(rot);
+      wrap_pending = true;
+    }
+  }
   if (S > 0) seek();
   // plans of the next stage's loads (into LDS slot `slot`); advances the cursor
   typename LA::Plan pa;
@@ -386,10 +396,15 @@ void gemm_dma_kernel(const GemmParams p) {
     pb = lb.plan(b_nxt, k_left, dst + A_BYTES, live);
     if (++cur_kt == KS) {
       cur_kt = 0;
-      ++cur_r;
-      if (cur_r < p.red_count) {
-        red_offsets(cur_r);
+      if (wrap_pending) {
+        wrap_pending = false;
         seek();
+      } else {
+        ++cur_r;
+        if (cur_r < p.red_count) {
+          red_offsets(cur_r);
+          seek();
+        }
       }
     } else {
       a_nxt += a_step;

@@ -50,6 +50,10 @@ struct GemmParams {
   float* z;
   int64_t ldz;
   int32_t act;
+  // DMA kernel, plain products (no split, no summed batch axes): blocks on
+  // XCD x start their K loop at stage x * KS / 8 and wrap around, so that the
+  // eight XCDs stream different columns of the operands at any one time
+  int32_t krot;
 };
 
 }  // namespace mt

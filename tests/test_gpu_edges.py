@@ -100,3 +100,36 @@ def test_long_row_pitch_few_rows():
     torch.cuda.synchronize()
     Yr, S = oracle.linear_fwd(to_f64(x), to_f64(w), None)
     assert_close(to_f64(y), Yr, S, what="Y (long pitch, few rows)")
+
+
+@pytest.mark.parametrize("krot", [0, 1])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_dma_tile_k_rotation_settings(krot, dtype):
+    """4096^2 outputs (the 256x256 DMA tile) with K = 1000 (a K tail): every
+    block starting at k = 0, and blocks starting at an XCD-dependent stage
+    and wrapping around; sampled against the oracle, reruns bit-identical."""
+    M = N = 4096
+    K = 1000
+    inp = wl.linear(M, N, K, dtype=dtype, seed=krot, dist={"X": ("normal",), "W": ("uniform", 1 / 32),
+                                                           "dY": ("normal",)}).make()
+    x, w, bias, dy = (inp[k].to(DEV) for k in ("X", "W", "b", "dY"))
+    b.debug_set("krot", krot)
+    try:
+        outs = []
+        for _ in range(2):
+            y = torch.full((M, N), float("nan"), device=DEV)
+            dw = torch.full((N, K), float("nan"), device=DEV)
+            b.linear_fwd(x, w, bias, y)
+            b.linear_bwd(x, w, dy, None, dw, None)
+            torch.cuda.synchronize()
+            outs.append((y, dw))
+    finally:
+        b.debug_set("krot", 1)
+    assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+    X, W, B, dY = (to_f64(inp[k]) for k in ("X", "W", "b", "dY"))
+    r, c = sample_positions(M, N, 2000, seed=krot)
+    want, S = oracle.linear_fwd_at(X, W, B, r, c)
+    assert_close(to_f64(outs[0][0])[r, c], want, S, what="Y")
+    r, c = sample_positions(N, K, 2000, seed=krot + 7)
+    want, S = oracle.linear_bwd_dw_at(dY, X, r, c)
+    assert_close(to_f64(outs[0][1])[r, c], want, S, what="dW")
