@@ -13,7 +13,7 @@ parity tolerances are scaled by.
 
 Paper passages (MiniTensor): Sec. 3.1 Eq. (1) matmul and the broadcasting
 rule; Sec. 3.2 Eq. (4) matmul pullbacks and the add pullback; Sec. 3.3
-Eq. (5) dense layer. bf16 inputs are widened bit-exactly (bits << 16 is the
+Eq. (5) dense layer; Sec. 3.3 Eq. (6) 2-D convolution and its pullbacks. bf16 inputs are widened bit-exactly (bits << 16 is the
 fp32 value), see :func:`bf16_bits_to_f64`.
 """
 from __future__ import annotations
@@ -70,6 +70,13 @@ def _load():
     for f in (lib.or_broadcast_shape, lib.or_matmul_shape, lib.or_matmul, lib.or_matmul_bwd,
               lib.or_reduce_broadcast, lib.or_num_threads):
         f.restype = ctypes.c_int
+    lib.or_conv2d_fwd.argtypes = [_I64, d, d, d, d, d]
+    lib.or_conv2d_bwd_dx.argtypes = [_I64, d, d, d, d]
+    lib.or_conv2d_bwd_dw.argtypes = [_I64, d, d, d, d]
+    lib.or_conv2d_bwd_db.argtypes = [_I64, d, d, d]
+    lib.or_conv2d_fwd_at.argtypes = [_I64, d, d, d, i64, _I64, d, d]
+    lib.or_conv2d_bwd_dx_at.argtypes = [_I64, d, d, i64, _I64, d, d]
+    lib.or_conv2d_bwd_dw_at.argtypes = [_I64, d, d, i64, _I64, d, d]
     _lib = lib
     return lib
 
@@ -285,3 +292,114 @@ def reduce_broadcast(g_out, in_shape):
     if r:
         raise ValueError(_SHAPE_ERRORS.get(r, str(r)))
     return gin, S
+
+
+# ----------------------------------------------------------- convolution --
+# Sec. 3.3 Eq. (6): 2-D convolution (cross-correlation as written there) with
+# stride (sh, sw) and zero padding (ph, pw), batched; NCHW arrays, 0-based
+# indices. Output size Ho = (H + 2 ph - KH) // sh + 1 (likewise Wo).
+
+def conv2d_out_hw(H, W, KH, KW, stride, pad):
+    sh, sw = stride
+    ph, pw = pad
+    return (H + 2 * ph - KH) // sh + 1, (W + 2 * pw - KW) // sw + 1
+
+
+def _conv_dims(xshape, wshape, stride, pad):
+    N, C, H, W = (int(v) for v in xshape)
+    CO, C2, KH, KW = (int(v) for v in wshape)
+    assert C2 == C, (xshape, wshape)
+    sh, sw = (int(v) for v in stride)
+    ph, pw = (int(v) for v in pad)
+    assert sh >= 1 and sw >= 1 and ph >= 0 and pw >= 0
+    HO, WO = conv2d_out_hw(H, W, KH, KW, stride, pad)
+    assert HO >= 1 and WO >= 1
+    dims = np.ascontiguousarray([N, C, H, W, CO, KH, KW, sh, sw, ph, pw], dtype=np.int64)
+    return dims, (N, CO, HO, WO)
+
+
+def conv2d_fwd(x, w, b, stride=(1, 1), pad=(0, 0)):
+    """y = conv(x, w) + b per Eq. (6). Returns (y, S)."""
+    x, w = _f64(x), _f64(w)
+    bb = None if b is None else _f64(b)
+    dims, yshape = _conv_dims(x.shape, w.shape, stride, pad)
+    y, S = np.empty(yshape), np.empty(yshape)
+    _load().or_conv2d_fwd(dims.ctypes.data_as(_I64), _p(x), _p(w), _p(bb), _p(y), _p(S))
+    return y, S
+
+
+def conv2d_bwd_dx(dy, w, xshape, stride=(1, 1), pad=(0, 0)):
+    """Pullback to the input. Returns (dx, S)."""
+    dy, w = _f64(dy), _f64(w)
+    dims, yshape = _conv_dims(xshape, w.shape, stride, pad)
+    assert dy.shape == yshape, (dy.shape, yshape)
+    dx, S = np.empty(tuple(xshape)), np.empty(tuple(xshape))
+    _load().or_conv2d_bwd_dx(dims.ctypes.data_as(_I64), _p(dy), _p(w), _p(dx), _p(S))
+    return dx, S
+
+
+def conv2d_bwd_dw(dy, x, wshape, stride=(1, 1), pad=(0, 0)):
+    """Pullback to the weights. Returns (dw, S)."""
+    dy, x = _f64(dy), _f64(x)
+    dims, yshape = _conv_dims(x.shape, wshape, stride, pad)
+    assert dy.shape == yshape, (dy.shape, yshape)
+    dw, S = np.empty(tuple(wshape)), np.empty(tuple(wshape))
+    _load().or_conv2d_bwd_dw(dims.ctypes.data_as(_I64), _p(dy), _p(x), _p(dw), _p(S))
+    return dw, S
+
+
+def conv2d_bwd_db(dy):
+    """Pullback to the bias: sums over n, i, j. Returns (db, S)."""
+    dy = _f64(dy)
+    N, CO, HO, WO = dy.shape
+    dims = np.ascontiguousarray([N, 1, 1, 1, CO, 1, 1, 1, 1, 0, 0], dtype=np.int64)
+    # with H = W = 1, KH = KW = 1 the dims only serve N, CO; Ho, Wo come from dy
+    dims[2], dims[3] = HO, WO
+    db, S = np.empty(CO), np.empty(CO)
+    _load().or_conv2d_bwd_db(dims.ctypes.data_as(_I64), _p(dy), _p(db), _p(S))
+    return db, S
+
+
+def _flat(idx):
+    f = np.ascontiguousarray(idx, dtype=np.int64)
+    assert f.ndim == 1
+    return f
+
+
+def conv2d_fwd_at(x, w, b, flat, stride=(1, 1), pad=(0, 0)):
+    """y.flat[flat[t]] and its S, one sampled element at a time."""
+    x, w = _f64(x), _f64(w)
+    bb = None if b is None else _f64(b)
+    dims, yshape = _conv_dims(x.shape, w.shape, stride, pad)
+    f = _flat(flat)
+    assert (f >= 0).all() and (f < np.prod(yshape)).all()
+    out, S = np.empty(len(f)), np.empty(len(f))
+    _load().or_conv2d_fwd_at(dims.ctypes.data_as(_I64), _p(x), _p(w), _p(bb), len(f),
+                             f.ctypes.data_as(_I64), _p(out), _p(S))
+    return out, S
+
+
+def conv2d_bwd_dx_at(dy, w, xshape, flat, stride=(1, 1), pad=(0, 0)):
+    """dx.flat[flat[t]] and its S."""
+    dy, w = _f64(dy), _f64(w)
+    dims, yshape = _conv_dims(xshape, w.shape, stride, pad)
+    assert dy.shape == yshape
+    f = _flat(flat)
+    assert (f >= 0).all() and (f < np.prod(xshape)).all()
+    out, S = np.empty(len(f)), np.empty(len(f))
+    _load().or_conv2d_bwd_dx_at(dims.ctypes.data_as(_I64), _p(dy), _p(w), len(f),
+                                f.ctypes.data_as(_I64), _p(out), _p(S))
+    return out, S
+
+
+def conv2d_bwd_dw_at(dy, x, wshape, flat, stride=(1, 1), pad=(0, 0)):
+    """dw.flat[flat[t]] and its S."""
+    dy, x = _f64(dy), _f64(x)
+    dims, yshape = _conv_dims(x.shape, wshape, stride, pad)
+    assert dy.shape == yshape
+    f = _flat(flat)
+    assert (f >= 0).all() and (f < np.prod(wshape)).all()
+    out, S = np.empty(len(f)), np.empty(len(f))
+    _load().or_conv2d_bwd_dw_at(dims.ctypes.data_as(_I64), _p(dy), _p(x), len(f),
+                                f.ctypes.data_as(_I64), _p(out), _p(S))
+    return out, S

@@ -9,6 +9,8 @@
 //   * Sec. 3.1, Eq. (1):     Y = X W^T                          (matmul)
 //   * Sec. 3.3, Eq. (5):     Dense(x; W, b) = x W^T + 1 b^T      (linear)
 //   * Sec. 3.2, Eq. (4):     Xbar += Ybar W,  Wbar += Ybar^T X   (pullbacks)
+//   * Sec. 3.3, Eq. (6):     2-D convolution with stride and zero padding,
+//                            and its pullbacks to the input, weights, bias
 //   * Sec. 3.2, add pullback: xbar += zbar, ybar += zbar; with the
 //     broadcasting rule of Sec. 3.1 this gives db = 1^T dY and, for
 //     broadcast batch axes, a sum of the gradient over those axes.
@@ -120,6 +122,106 @@ void unflatten(int64_t flat, int n, const int64_t* shape, int64_t* idx) {
     idx[i] = shape[i] ? flat % shape[i] : 0;
     flat = shape[i] ? flat / shape[i] : 0;
   }
+}
+
+}  // namespace
+
+namespace {
+
+// ------------------------------------------------------------ convolution
+//
+// Sec. 3.3 Eq. (6), 2-D convolution with stride (sh, sw) and zero padding
+// (ph, pw), batched over n, all indices 0-based, tensors in NCHW order:
+//   y[n][c][i][j] = sum_{c'} sum_{u} sum_{v} w[c][c'][u][v] x[n][c'][i sh + u - ph][j sw + v - pw]
+//                   (+ b[c]), x read as 0 outside the image;
+//   Ho = (H + 2 ph - KH) / sh + 1, Wo = (W + 2 pw - KW) / sw + 1.
+// Pullbacks (the matmul pullbacks of Eq. (4) through the linear map of
+// Eq. (6)): each term w x of some y is charged to both factors,
+//   dx[n][c'][h][x]  = sum over (c, u, v) with h = i sh + u - ph, x = j sw + v - pw
+//                      of dy[n][c][i][j] w[c][c'][u][v],
+//   dw[c][c'][u][v]  = sum over (n, i, j) of dy[n][c][i][j] x[n][c'][i sh + u - ph][j sw + v - pw],
+//   db[c]            = sum over (n, i, j) of dy[n][c][i][j].
+// Each element is one fp64 sum in the order of the indices as written
+// (outermost first), with S = sum of |term| beside it.
+
+struct ConvDims {
+  int64_t N, C, H, W, CO, KH, KW, sh, sw, ph, pw, HO, WO;
+};
+
+ConvDims conv_dims(const int64_t* d) {
+  ConvDims c;
+  c.N = d[0]; c.C = d[1]; c.H = d[2]; c.W = d[3]; c.CO = d[4]; c.KH = d[5]; c.KW = d[6];
+  c.sh = d[7]; c.sw = d[8]; c.ph = d[9]; c.pw = d[10];
+  c.HO = (c.H + 2 * c.ph - c.KH) / c.sh + 1;
+  c.WO = (c.W + 2 * c.pw - c.KW) / c.sw + 1;
+  return c;
+}
+
+void conv_y_elem(const ConvDims& c, const double* x, const double* w, const double* b,
+                 int64_t n, int64_t co, int64_t i, int64_t j, double* out, double* S) {
+  double acc = 0.0, s = 0.0;
+  for (int64_t ci = 0; ci < c.C; ++ci)
+    for (int64_t u = 0; u < c.KH; ++u)
+      for (int64_t v = 0; v < c.KW; ++v) {
+        const int64_t h = i * c.sh + u - c.ph, xx = j * c.sw + v - c.pw;
+        if (h < 0 || h >= c.H || xx < 0 || xx >= c.W) continue;
+        const double p = w[((co * c.C + ci) * c.KH + u) * c.KW + v] *
+                         x[((n * c.C + ci) * c.H + h) * c.W + xx];
+        acc += p;
+        s += std::fabs(p);
+      }
+  if (b) {
+    acc += b[co];
+    s += std::fabs(b[co]);
+  }
+  *out = acc;
+  *S = s;
+}
+
+void conv_dx_elem(const ConvDims& c, const double* dy, const double* w, int64_t n, int64_t ci,
+                  int64_t h, int64_t xx, double* out, double* S) {
+  double acc = 0.0, s = 0.0;
+  for (int64_t co = 0; co < c.CO; ++co)
+    for (int64_t u = 0; u < c.KH; ++u)
+      for (int64_t v = 0; v < c.KW; ++v) {
+        const int64_t ti = h + c.ph - u, tj = xx + c.pw - v;   // = i sh, j sw
+        if (ti < 0 || tj < 0 || ti % c.sh || tj % c.sw) continue;
+        const int64_t i = ti / c.sh, j = tj / c.sw;
+        if (i >= c.HO || j >= c.WO) continue;
+        const double p = dy[((n * c.CO + co) * c.HO + i) * c.WO + j] *
+                         w[((co * c.C + ci) * c.KH + u) * c.KW + v];
+        acc += p;
+        s += std::fabs(p);
+      }
+  *out = acc;
+  *S = s;
+}
+
+void conv_dw_elem(const ConvDims& c, const double* dy, const double* x, int64_t co, int64_t ci,
+                  int64_t u, int64_t v, double* out, double* S) {
+  double acc = 0.0, s = 0.0;
+  for (int64_t n = 0; n < c.N; ++n)
+    for (int64_t i = 0; i < c.HO; ++i)
+      for (int64_t j = 0; j < c.WO; ++j) {
+        const int64_t h = i * c.sh + u - c.ph, xx = j * c.sw + v - c.pw;
+        if (h < 0 || h >= c.H || xx < 0 || xx >= c.W) continue;
+        const double p = dy[((n * c.CO + co) * c.HO + i) * c.WO + j] *
+                         x[((n * c.C + ci) * c.H + h) * c.W + xx];
+        acc += p;
+        s += std::fabs(p);
+      }
+  *out = acc;
+  *S = s;
+}
+
+void unflat4(int64_t f, int64_t d1, int64_t d2, int64_t d3, int64_t* a, int64_t* b_, int64_t* c_,
+             int64_t* e) {
+  *e = f % d3;
+  f /= d3;
+  *c_ = f % d2;
+  f /= d2;
+  *b_ = f % d1;
+  *a = f / d1;
 }
 
 }  // namespace
@@ -417,6 +519,103 @@ int or_reduce_broadcast(int nout_dims, const int64_t* oshape, const double* gout
     S[j] += std::fabs(gout[f]);
   }
   return OR_OK;
+}
+
+
+// dims = {N, C, H, W, CO, KH, KW, sh, sw, ph, pw}; every tensor NCHW-contiguous fp64.
+void or_conv2d_fwd(const int64_t* dims, const double* x, const double* w, const double* b,
+                   double* y, double* S) {
+  const ConvDims c = conv_dims(dims);
+  const int64_t rows = c.N * c.CO;
+#pragma omp parallel for schedule(dynamic)
+  for (int64_t r = 0; r < rows; ++r) {
+    const int64_t n = r / c.CO, co = r % c.CO;
+    for (int64_t i = 0; i < c.HO; ++i)
+      for (int64_t j = 0; j < c.WO; ++j) {
+        const int64_t f = ((n * c.CO + co) * c.HO + i) * c.WO + j;
+        conv_y_elem(c, x, w, b, n, co, i, j, &y[f], &S[f]);
+      }
+  }
+}
+
+void or_conv2d_bwd_dx(const int64_t* dims, const double* dy, const double* w, double* dx,
+                      double* S) {
+  const ConvDims c = conv_dims(dims);
+  const int64_t rows = c.N * c.C;
+#pragma omp parallel for schedule(dynamic)
+  for (int64_t r = 0; r < rows; ++r) {
+    const int64_t n = r / c.C, ci = r % c.C;
+    for (int64_t h = 0; h < c.H; ++h)
+      for (int64_t xx = 0; xx < c.W; ++xx) {
+        const int64_t f = ((n * c.C + ci) * c.H + h) * c.W + xx;
+        conv_dx_elem(c, dy, w, n, ci, h, xx, &dx[f], &S[f]);
+      }
+  }
+}
+
+void or_conv2d_bwd_dw(const int64_t* dims, const double* dy, const double* x, double* dw,
+                      double* S) {
+  const ConvDims c = conv_dims(dims);
+  const int64_t rows = c.CO * c.C;
+#pragma omp parallel for schedule(dynamic)
+  for (int64_t r = 0; r < rows; ++r) {
+    const int64_t co = r / c.C, ci = r % c.C;
+    for (int64_t u = 0; u < c.KH; ++u)
+      for (int64_t v = 0; v < c.KW; ++v) {
+        const int64_t f = ((co * c.C + ci) * c.KH + u) * c.KW + v;
+        conv_dw_elem(c, dy, x, co, ci, u, v, &dw[f], &S[f]);
+      }
+  }
+}
+
+void or_conv2d_bwd_db(const int64_t* dims, const double* dy, double* db, double* S) {
+  const ConvDims c = conv_dims(dims);
+  for (int64_t co = 0; co < c.CO; ++co) {
+    double acc = 0.0, s = 0.0;
+    for (int64_t n = 0; n < c.N; ++n)
+      for (int64_t i = 0; i < c.HO; ++i)
+        for (int64_t j = 0; j < c.WO; ++j) {
+          const double g = dy[((n * c.CO + co) * c.HO + i) * c.WO + j];
+          acc += g;
+          s += std::fabs(g);
+        }
+    db[co] = acc;
+    S[co] = s;
+  }
+}
+
+// Sampled elements: flat NCHW indices into y / dx / dw.
+void or_conv2d_fwd_at(const int64_t* dims, const double* x, const double* w, const double* b,
+                      int64_t cnt, const int64_t* flat, double* out, double* S) {
+  const ConvDims c = conv_dims(dims);
+#pragma omp parallel for schedule(dynamic)
+  for (int64_t t = 0; t < cnt; ++t) {
+    int64_t n, co, i, j;
+    unflat4(flat[t], c.CO, c.HO, c.WO, &n, &co, &i, &j);
+    conv_y_elem(c, x, w, b, n, co, i, j, &out[t], &S[t]);
+  }
+}
+
+void or_conv2d_bwd_dx_at(const int64_t* dims, const double* dy, const double* w, int64_t cnt,
+                         const int64_t* flat, double* out, double* S) {
+  const ConvDims c = conv_dims(dims);
+#pragma omp parallel for schedule(dynamic)
+  for (int64_t t = 0; t < cnt; ++t) {
+    int64_t n, ci, h, xx;
+    unflat4(flat[t], c.C, c.H, c.W, &n, &ci, &h, &xx);
+    conv_dx_elem(c, dy, w, n, ci, h, xx, &out[t], &S[t]);
+  }
+}
+
+void or_conv2d_bwd_dw_at(const int64_t* dims, const double* dy, const double* x, int64_t cnt,
+                         const int64_t* flat, double* out, double* S) {
+  const ConvDims c = conv_dims(dims);
+#pragma omp parallel for schedule(dynamic)
+  for (int64_t t = 0; t < cnt; ++t) {
+    int64_t co, ci, u, v;
+    unflat4(flat[t], c.C, c.KH, c.KW, &co, &ci, &u, &v);
+    conv_dw_elem(c, dy, x, co, ci, u, v, &out[t], &S[t]);
+  }
 }
 
 }  // extern "C"

@@ -95,3 +95,37 @@ def test_nn_pins_catch_mutant(tmp_path, name, old, new):
                         os.path.join(HERE, "test_oracle_nn.py")], cwd=ROOT, env=env,
                        capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the oracle pins:\n{r.stdout[-2000:]}"
+
+
+# planted mistakes in the convolution part of oracle/oracle.cpp, caught by test_oracle_conv.py
+MUTANTS_CONV = [
+    ("conv_padding_sign", "  double acc = 0.0, s = 0.0;\n  for (int64_t ci = 0; ci < c.C; ++ci)\n    for (int64_t u = 0; u < c.KH; ++u)\n      for (int64_t v = 0; v < c.KW; ++v) {\n        const int64_t h = i * c.sh + u - c.ph,",
+     "  double acc = 0.0, s = 0.0;\n  for (int64_t ci = 0; ci < c.C; ++ci)\n    for (int64_t u = 0; u < c.KH; ++u)\n      for (int64_t v = 0; v < c.KW; ++v) {\n        const int64_t h = i * c.sh + u + c.ph,"),
+    ("conv_kernel_flipped", "        const double p = w[((co * c.C + ci) * c.KH + u) * c.KW + v] *\n                         x[((n * c.C + ci) * c.H + h) * c.W + xx];",
+     "        const double p = w[((co * c.C + ci) * c.KH + (c.KH - 1 - u)) * c.KW + v] *\n                         x[((n * c.C + ci) * c.H + h) * c.W + xx];"),
+    ("conv_dx_ignores_stride_phase", "        if (ti < 0 || tj < 0 || ti % c.sh || tj % c.sw) continue;",
+     "        if (ti < 0 || tj < 0) continue;"),
+    ("conv_dw_kernel_axes_swapped", "        const int64_t h = i * c.sh + u - c.ph, xx = j * c.sw + v - c.pw;\n        if (h < 0 || h >= c.H || xx < 0 || xx >= c.W) continue;\n        const double p = dy[((n * c.CO + co) * c.HO + i) * c.WO + j] *",
+     "        const int64_t h = i * c.sh + v - c.ph, xx = j * c.sw + u - c.pw;\n        if (h < 0 || h >= c.H || xx < 0 || xx >= c.W) continue;\n        const double p = dy[((n * c.CO + co) * c.HO + i) * c.WO + j] *"),
+    ("conv_db_skips_first_image", "    for (int64_t n = 0; n < c.N; ++n)\n      for (int64_t i = 0; i < c.HO; ++i)\n        for (int64_t j = 0; j < c.WO; ++j) {\n          const double g",
+     "    for (int64_t n = 1; n < c.N; ++n)\n      for (int64_t i = 0; i < c.HO; ++i)\n        for (int64_t j = 0; j < c.WO; ++j) {\n          const double g"),
+    ("conv_output_size_floor_off", "  c.HO = (c.H + 2 * c.ph - c.KH) / c.sh + 1;", "  c.HO = (c.H + 2 * c.ph - c.KH + c.sh - 1) / c.sh + 1;"),
+    ("conv_bias_dropped", "  if (b) {\n    acc += b[co];\n    s += std::fabs(b[co]);\n  }\n  *out = acc;",
+     "  if (b) {\n    s += std::fabs(b[co]);\n  }\n  *out = acc;"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS_CONV, ids=[m[0] for m in MUTANTS_CONV])
+def test_conv_pins_catch_mutant(tmp_path, name, old, new):
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} not unique/found"
+    mutated = tmp_path / "oracle_mut.cpp"
+    mutated.write_text(src.replace(old, new))
+    lib = tmp_path / "liboracle_mut.so"
+    subprocess.run(["g++", "-std=c++17", "-O1", "-fopenmp", "-ffp-contract=off", "-fPIC", "-shared",
+                    "-o", str(lib), str(mutated)], check=True)
+    env = dict(os.environ, MT_ORACLE_LIB_OVERRIDE=str(lib), OMP_NUM_THREADS="2")
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(HERE, "test_oracle_conv.py")], cwd=ROOT, env=env,
+                       capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"mutant {name} survived the oracle pins:\n{r.stdout[-2000:]}"
