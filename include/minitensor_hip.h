@@ -20,7 +20,8 @@
  *     Workspace, where an entry point takes one, is caller-supplied device
  *     memory; its required size comes from the matching *_workspace call.
  *     A NULL workspace (or one that is too small) selects a slower variant
- *     that needs none, so workspace only ever buys speed.
+ *     that needs none, so workspace only ever buys speed (the convolution,
+ *     whose unfolded input lives there, is the one exception).
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *     All device work is enqueued on it asynchronously; results are visible
  *     after the caller synchronises that stream.
@@ -200,6 +201,53 @@ mt_status mt_adam_step(int32_t n, const mt_tensor* params, const mt_tensor* grad
  */
 mt_status mt_rmsprop_step(int32_t n, const mt_tensor* params, const mt_tensor* grads,
                           const mt_tensor* sq_avg, float lr, float alpha, float eps, void* stream);
+
+/* ----------------------------------------------------------- convolution
+ * 2-D convolution of Sec. 3.3 Eq. (6), batched, with stride (stride_h,
+ * stride_w) and zero padding (pad_h, pad_w), 0-based indices:
+ *   y[n][c][i][j] = sum_{c', u, v} w[c][c'][u][v] x[n][c'][i sh + u - ph][j sw + v - pw] + b[c]
+ *   (x read as 0 outside the image), Ho = (H + 2 ph - KH) / sh + 1, likewise Wo.
+ * Shapes are given in [N][C][H][W] order whatever the memory layout:
+ *   x  [N, C, H, W]    f32, any strides (read through them)
+ *   w  [CO, C, KH, KW] f32; the taps of one output channel contiguous, either
+ *                      as [C][KH][KW] (the usual layout) or channels-last
+ *                      [KH][KW][C]; any pitch between output channels
+ *   b  [CO] f32 or NULL;  y [N, CO, Ho, Wo] f32 channels-last contiguous
+ *                      (memory order N, Ho, Wo, CO)
+ * The convolution runs as a product of the unfolded input (a row per output
+ * pixel, a column per tap) with the flattened weights on the matrix cores.
+ * The unfolded input lives in the caller's workspace, which is therefore
+ * REQUIRED here (MT_ERR_WORKSPACE without it; size from the *_workspace
+ * call: N Ho Wo x round_up(C KH KW, 4) floats, plus split-K partials for dw).
+ * fp32 only.
+ */
+mt_status mt_conv2d_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* b,
+                        const mt_tensor* y, int32_t stride_h, int32_t stride_w, int32_t pad_h,
+                        int32_t pad_w, void* ws, size_t ws_bytes, void* stream);
+mt_status mt_conv2d_fwd_workspace(const mt_tensor* x, const mt_tensor* w, const mt_tensor* b,
+                                  const mt_tensor* y, int32_t stride_h, int32_t stride_w,
+                                  int32_t pad_h, int32_t pad_w, size_t* bytes);
+
+/* mt_conv2d_bwd: the pullbacks of Eq. (6) from dy (the matmul pullbacks of
+ * Eq. (4) through the unfolded form, and the add pullback for b):
+ *   dx[n][c'][h][x] = sum of dy[n][c][i][j] w[c][c'][u][v] over the (c, i, j, u, v)
+ *                     with h = i sh + u - ph, x = j sw + v - pw   (NULL to skip)
+ *   dw[c][c'][u][v] = sum over (n, i, j) of dy[n][c][i][j] x[n][c'][i sh + u - ph][j sw + v - pw]
+ *   db[c]           = sum over (n, i, j) of dy[n][c][i][j]
+ *   dy [N, CO, Ho, Wo] channels-last contiguous; dx [N, C, H, W] contiguous,
+ *   channels-last or [N][C][H][W]; dw the shape of w with its taps in w's
+ *   order; db [CO]. x and w are needed for their shapes (and x's data for
+ *   dw, w's data for dx). flags: MT_ACCUMULATE. The input gradient is a
+ *   gather over the taps that read each element: no atomics, deterministic.
+ */
+mt_status mt_conv2d_bwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* dy,
+                        const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db,
+                        int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                        uint32_t flags, void* ws, size_t ws_bytes, void* stream);
+mt_status mt_conv2d_bwd_workspace(const mt_tensor* x, const mt_tensor* w, const mt_tensor* dy,
+                                  const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db,
+                                  int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                                  size_t* bytes);
 
 /* -------------------------------------------------------------- matmul
  * mt_matmul: C = A @ B with NumPy/PyTorch matmul semantics (Eq. (1) per

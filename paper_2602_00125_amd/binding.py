@@ -31,7 +31,8 @@ EXPORTS = ["mt_linear_fwd", "mt_linear_bwd", "mt_linear_bwd_workspace", "mt_matm
            "mt_reduce_broadcast_grad", "mt_reduce_broadcast_grad_workspace", "mt_broadcast_shape",
            "mt_matmul_shape", "mt_debug_set", "mt_status_str", "mt_last_error",
            "mt_linear_act_fwd", "mt_act_bwd", "mt_act_bwd_workspace", "mt_mse_loss",
-           "mt_mse_loss_workspace", "mt_sgd_step", "mt_adam_step", "mt_rmsprop_step"]
+           "mt_mse_loss_workspace", "mt_sgd_step", "mt_adam_step", "mt_rmsprop_step",
+           "mt_conv2d_fwd", "mt_conv2d_fwd_workspace", "mt_conv2d_bwd", "mt_conv2d_bwd_workspace"]
 ACT = {"none": 0, "relu": 1, "sigmoid": 2, "tanh": 3, "gelu": 4}
 
 
@@ -62,6 +63,12 @@ _f = ctypes.c_float
 lib.mt_sgd_step.argtypes = [ctypes.c_int32, _P, _P, _P, _f, _f, _f, _vp]
 lib.mt_adam_step.argtypes = [ctypes.c_int32, _P, _P, _P, _P, _f, _f, _f, _f, ctypes.c_int64, _vp]
 lib.mt_rmsprop_step.argtypes = [ctypes.c_int32, _P, _P, _P, _f, _f, _f, _vp]
+_i32 = ctypes.c_int32
+lib.mt_conv2d_fwd.argtypes = [_P, _P, _P, _P, _i32, _i32, _i32, _i32, _vp, _sz, _vp]
+lib.mt_conv2d_fwd_workspace.argtypes = [_P, _P, _P, _P, _i32, _i32, _i32, _i32, ctypes.POINTER(_sz)]
+lib.mt_conv2d_bwd.argtypes = [_P, _P, _P, _P, _P, _P, _i32, _i32, _i32, _i32, _u32, _vp, _sz, _vp]
+lib.mt_conv2d_bwd_workspace.argtypes = [_P, _P, _P, _P, _P, _P, _i32, _i32, _i32, _i32,
+                                        ctypes.POINTER(_sz)]
 lib.mt_debug_set.argtypes = [ctypes.c_char_p, ctypes.c_int64]
 lib.mt_status_str.argtypes = [ctypes.c_int]
 lib.mt_status_str.restype = ctypes.c_char_p
@@ -261,6 +268,47 @@ def rmsprop_step(params, grads, sq_avg, lr, alpha, eps, stream=None) -> None:
     assert len(grads) == n and len(sq_avg) == n
     _check(lib.mt_rmsprop_step(n, _desc_array(params), _desc_array(grads), _desc_array(sq_avg),
                                lr, alpha, eps, _stream(stream)), "mt_rmsprop_step")
+
+
+def _pair(v):
+    return (int(v), int(v)) if isinstance(v, int) else (int(v[0]), int(v[1]))
+
+
+def conv2d_fwd_workspace(x, w, b, y, stride=1, padding=0) -> int:
+    n = _sz(0)
+    st, pd = _pair(stride), _pair(padding)
+    ds = [desc(t) for t in (x, w, b, y)]
+    _check(lib.mt_conv2d_fwd_workspace(*[_ref(d) for d in ds], *st, *pd, ctypes.byref(n)),
+           "mt_conv2d_fwd_workspace")
+    return int(n.value)
+
+
+def conv2d_fwd(x, w, b, y, stride=1, padding=0, workspace=None, stream=None) -> None:
+    """y = conv2d(x, w) + b (Eq. (6)); y channels-last [N, CO, Ho, Wo]."""
+    st, pd = _pair(stride), _pair(padding)
+    ds = [desc(t) for t in (x, w, b, y)]
+    ptr, nbytes = _ws(workspace)
+    _check(lib.mt_conv2d_fwd(*[_ref(d) for d in ds], *st, *pd, ptr, nbytes, _stream(stream)),
+           "mt_conv2d_fwd")
+
+
+def conv2d_bwd_workspace(x, w, dy, dx=None, dw=None, db=None, stride=1, padding=0) -> int:
+    n = _sz(0)
+    st, pd = _pair(stride), _pair(padding)
+    ds = [desc(t) for t in (x, w, dy, dx, dw, db)]
+    _check(lib.mt_conv2d_bwd_workspace(*[_ref(d) for d in ds], *st, *pd, ctypes.byref(n)),
+           "mt_conv2d_bwd_workspace")
+    return int(n.value)
+
+
+def conv2d_bwd(x, w, dy, dx=None, dw=None, db=None, stride=1, padding=0, accumulate=False,
+               workspace=None, stream=None) -> None:
+    """Pullbacks of conv2d: dx, dw, db (None skips one)."""
+    st, pd = _pair(stride), _pair(padding)
+    ds = [desc(t) for t in (x, w, dy, dx, dw, db)]
+    ptr, nbytes = _ws(workspace)
+    _check(lib.mt_conv2d_bwd(*[_ref(d) for d in ds], *st, *pd, ACCUMULATE if accumulate else 0,
+                             ptr, nbytes, _stream(stream)), "mt_conv2d_bwd")
 
 
 def _shape_call(fn, a, b, where):

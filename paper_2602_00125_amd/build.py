@@ -17,8 +17,8 @@ OUT = os.path.join(HERE, "libminitensor_hip.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["gemm_f32.hip", "gemm_bf16.hip", "reduce.hip", "elementwise.hip", "shape.cpp",
-           "capi.cpp"]
+SOURCES = ["gemm_f32.hip", "gemm_bf16.hip", "reduce.hip", "elementwise.hip", "conv.hip",
+           "shape.cpp", "capi.cpp"]
 COMMON = ["-std=c++17", "-O3", "-fPIC", "-Wall", "-Wno-unused-result",
           f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-I", os.path.join(HERE, "..", "include")]

@@ -709,6 +709,259 @@ mt_status plan_opt(int32_t n, const mt_tensor* params, const mt_tensor* grads,
   return MT_OK;
 }
 
+
+// ---------------------------------------------------------- convolution
+struct ConvPlan {
+  mt::ConvGeom g;
+  int64_t M;         // output pixels N HO WO (rows of the unfolded matrix)
+  int64_t wpitch;    // row pitch of the flattened weights [CO][Kc]
+  size_t col_bytes;  // the unfolded matrix in the workspace, rounded up to 256
+};
+
+// dims `perm` (innermost first) of t form one dense row-major block
+bool dense_block(const mt_tensor* t, const int* perm, int n) {
+  int64_t expect = 1;
+  for (int i = 0; i < n; ++i) {
+    const int d = perm[i];
+    if (t->shape[d] != 1 && t->stride[d] != expect) return false;
+    expect *= t->shape[d];
+  }
+  return true;
+}
+
+// [N][C][H][W] stored channels-last: C fastest, then W, H, N, no gaps
+bool channels_last(const mt_tensor* t) {
+  static const int perm[4] = {1, 3, 2, 0};
+  return dense_block(t, perm, 4);
+}
+
+mt_status conv_plan(const mt_tensor* x, const mt_tensor* w, int32_t sh, int32_t sw, int32_t ph,
+                    int32_t pw, ConvPlan* cp) {
+  mt_status s;
+  if ((s = check_tensor(x, "x", 4, 4)) || (s = check_tensor(w, "w", 4, 4))) return s;
+  if (x->dtype != MT_F32 || w->dtype != MT_F32)
+    return fail(MT_ERR_DTYPE, "convolution: x and w must be f32");
+  if (sh < 1 || sw < 1 || ph < 0 || pw < 0)
+    return fail(MT_ERR_INVALID, "convolution: stride >= 1 and padding >= 0 required");
+  const int64_t N = x->shape[0], C = x->shape[1], H = x->shape[2], W = x->shape[3];
+  const int64_t CO = w->shape[0], KH = w->shape[2], KW = w->shape[3];
+  if (w->shape[1] != C) return fail(MT_ERR_SHAPE, "convolution: w[1] must equal x's channels");
+  if (C < 1 || H < 1 || W < 1 || CO < 1 || KH < 1 || KW < 1)
+    return fail(MT_ERR_SHAPE, "convolution: every size but the batch must be >= 1");
+  const int64_t lim = (int64_t)1 << 30;
+  if (N >= lim || C >= lim || H >= lim || W >= lim || CO >= lim || KH >= lim || KW >= lim ||
+      ph >= lim / 4 || pw >= lim / 4)
+    return fail(MT_ERR_SHAPE, "convolution: a size exceeds 2^30");
+  if (H + 2 * ph < KH || W + 2 * pw < KW)
+    return fail(MT_ERR_SHAPE, "convolution: the kernel is larger than the padded image");
+  const int64_t HO = (H + 2 * ph - KH) / sh + 1, WO = (W + 2 * pw - KW) / sw + 1;
+  static const int uvc[3] = {1, 3, 2};  // c fastest, then v, u
+  static const int cuv[3] = {3, 2, 1};  // v fastest, then u, c
+  int korder;
+  if (dense_block(w, cuv, 3)) korder = 0;
+  else if (dense_block(w, uvc, 3)) korder = 1;
+  else
+    return fail(MT_ERR_LAYOUT, "w: the taps of one output channel must be contiguous, "
+                               "[CO][C][KH][KW] or channels-last [CO][KH][KW][C]");
+  const int64_t Kc = C * KH * KW;
+  mt::ConvGeom& g = cp->g;
+  std::memset(&g, 0, sizeof(g));
+  g.N = (int32_t)N; g.C = (int32_t)C; g.H = (int32_t)H; g.W = (int32_t)W;
+  g.CO = (int32_t)CO; g.KH = (int32_t)KH; g.KW = (int32_t)KW;
+  g.sh = sh; g.sw = sw; g.ph = ph; g.pw = pw;
+  g.HO = (int32_t)HO; g.WO = (int32_t)WO;
+  g.korder_uvc = korder;
+  g.Kc = Kc;
+  g.Kcp = (Kc + 3) / 4 * 4;
+  for (int d = 0; d < 4; ++d) g.xs[d] = x->stride[d];
+  cp->M = N * HO * WO;
+  cp->wpitch = CO > 1 ? w->stride[0] : Kc;
+  if (cp->wpitch < Kc) return fail(MT_ERR_LAYOUT, "w: output channels overlap");
+  const int64_t bytes = cp->M * g.Kcp * 4;
+  cp->col_bytes = (size_t)((bytes + 255) / 256 * 256);
+  return MT_OK;
+}
+
+mt_status check_act4(const mt_tensor* t, const char* name, int64_t N, int64_t C, int64_t H,
+                     int64_t W) {
+  mt_status s = check_tensor(t, name, 4, 4);
+  if (s) return s;
+  if (t->dtype != MT_F32) return fail(MT_ERR_DTYPE, std::string(name) + ": must be f32");
+  if (t->shape[0] != N || t->shape[1] != C || t->shape[2] != H || t->shape[3] != W)
+    return fail(MT_ERR_SHAPE, std::string(name) + ": wrong shape");
+  return MT_OK;
+}
+
+mt_status conv_fwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor* b,
+                        const mt_tensor* y, int32_t sh, int32_t sw, int32_t ph, int32_t pw,
+                        void* ws, size_t ws_bytes, hipStream_t stream, size_t* ws_query) {
+  ConvPlan cp;
+  mt_status s = conv_plan(x, w, sh, sw, ph, pw, &cp);
+  if (s) return s;
+  const mt::ConvGeom& g = cp.g;
+  if ((s = check_act4(y, "y", g.N, g.CO, g.HO, g.WO))) return s;
+  if (!channels_last(y)) return fail(MT_ERR_LAYOUT, "y must be channels-last contiguous");
+  if (b && (s = check_vector(b, "b", g.CO))) return s;
+  if (overlaps(y, x) || overlaps(y, w) || overlaps(y, b))
+    return fail(MT_ERR_ALIAS, "y overlaps an input");
+  if (ws_query) {
+    *ws_query = cp.col_bytes;
+    return MT_OK;
+  }
+  if (cp.M == 0) return MT_OK;
+  if (!ws || ws_bytes < cp.col_bytes || ((uintptr_t)ws & 255))
+    return fail(MT_ERR_WORKSPACE, "convolution: needs a 256-byte aligned workspace of "
+                                  "mt_conv2d_fwd_workspace bytes (the unfolded input)");
+  float* col = (float*)ws;
+  (void)hipGetLastError();
+  if ((s = hip_status(mt::conv_unfold((const float*)x->data, g, col, stream)))) return s;
+  GemmCall gc{};
+  init_params(&gc.p);
+  gc.p.a = col;
+  gc.p.b = w->data;
+  gc.p.c = (float*)y->data;
+  gc.p.bias = b ? (const float*)b->data : nullptr;
+  gc.p.M = cp.M;
+  gc.p.N = g.CO;
+  gc.p.K = g.Kc;
+  gc.p.lda = g.Kcp;
+  gc.p.ldb = cp.wpitch;
+  gc.p.ldc = g.CO;
+  gc.a_kc = true;
+  gc.b_kc = true;
+  gc.bf16 = false;
+  gc.vec = g.Kc % 4 == 0 && vec_ok_operand(w->data, g.CO, g.Kc, cp.wpitch, nullptr, 0, 4) &&
+           aligned16(y->data) && g.CO % 4 == 0 && (!gc.p.bias || aligned16(gc.p.bias));
+  gc.cfg = -1;
+  return launch_gemm(gc, stream, nullptr, 0);
+}
+
+mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor* dy,
+                        const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db, int32_t sh,
+                        int32_t sw, int32_t ph, int32_t pw, uint32_t flags, void* ws,
+                        size_t ws_bytes, hipStream_t stream, size_t* ws_query) {
+  if (flags & ~MT_ACCUMULATE) return fail(MT_ERR_INVALID, "mt_conv2d_bwd: unknown flags");
+  ConvPlan cp;
+  mt_status s = conv_plan(x, w, sh, sw, ph, pw, &cp);
+  if (s) return s;
+  mt::ConvGeom& g = cp.g;
+  if ((s = check_act4(dy, "dy", g.N, g.CO, g.HO, g.WO))) return s;
+  if (!channels_last(dy)) return fail(MT_ERR_LAYOUT, "dy must be channels-last contiguous");
+  if (dx) {
+    if ((s = check_act4(dx, "dx", g.N, g.C, g.H, g.W))) return s;
+    if (!channels_last(dx) && !is_row_major(dx))
+      return fail(MT_ERR_LAYOUT, "dx must be contiguous, channels-last or [N][C][H][W]");
+    for (int d = 0; d < 4; ++d) g.ds[d] = dx->stride[d];
+    g.dx_vec = (g.C == 1 || dx->stride[1] == 1) && aligned16(dx->data) && dx->stride[0] % 4 == 0 &&
+               dx->stride[2] % 4 == 0 && dx->stride[3] % 4 == 0;
+  }
+  if (dw) {
+    s = check_tensor(dw, "dw", 4, 4);
+    if (s) return s;
+    if (dw->dtype != MT_F32) return fail(MT_ERR_DTYPE, "dw must be f32");
+    for (int d = 0; d < 4; ++d)
+      if (dw->shape[d] != w->shape[d]) return fail(MT_ERR_SHAPE, "dw must have w's shape");
+    static const int uvc[3] = {1, 3, 2};
+    static const int cuv[3] = {3, 2, 1};
+    if (!dense_block(dw, g.korder_uvc ? uvc : cuv, 3))
+      return fail(MT_ERR_LAYOUT, "dw must store the taps in w's order");
+    if (g.CO > 1 && dw->stride[0] < g.Kc) return fail(MT_ERR_LAYOUT, "dw: output channels overlap");
+  }
+  if (db && (s = check_vector(db, "db", g.CO))) return s;
+  const mt_tensor* ins[3] = {x, w, dy};
+  const mt_tensor* outs[3] = {dx, dw, db};
+  for (int i = 0; i < 3; ++i) {
+    if (!outs[i]) continue;
+    for (int j = 0; j < 3; ++j)
+      if (overlaps(outs[i], ins[j])) return fail(MT_ERR_ALIAS, "an output overlaps an input");
+    for (int j = i + 1; j < 3; ++j)
+      if (overlaps(outs[i], outs[j])) return fail(MT_ERR_ALIAS, "outputs overlap");
+  }
+  const bool acc = (flags & MT_ACCUMULATE) != 0;
+  const int64_t dwpitch = dw ? (g.CO > 1 ? dw->stride[0] : g.Kc) : 0;
+  // dW = dY^T U (U unfolded into the workspace), split over the pixels when its
+  // few output tiles under-fill the GPU; partial tiles go after U
+  GemmCall gdw{};
+  size_t need_dw = 0;
+  if (dw) {
+    init_params(&gdw.p);
+    gdw.p.a = dy->data;
+    gdw.p.b = ws;  // U, set again at launch
+    gdw.p.c = (float*)dw->data;
+    gdw.p.M = g.CO;
+    gdw.p.N = g.Kc;
+    gdw.p.K = cp.M;
+    gdw.p.lda = g.CO;
+    gdw.p.ldb = g.Kcp;
+    gdw.p.ldc = dwpitch;
+    gdw.p.accumulate = acc;
+    gdw.a_kc = false;
+    gdw.b_kc = false;
+    gdw.bf16 = false;
+    gdw.vec = g.CO % 4 == 0 && g.Kc % 4 == 0 && aligned16(dy->data) && aligned16(dw->data) &&
+              dwpitch % 4 == 0;
+    gdw.cfg = -1;
+    GemmCall probe = gdw;
+    need_dw = plan_gemm(probe, true);
+  }
+  int parts = 1;
+  size_t need_db = 0;
+  if (db && cp.M > 0) {
+    parts = g_force_parts > 0 ? g_force_parts : mt::colsum_parts(cp.M, g.CO);
+    if (parts > 1) need_db = (size_t)parts * g.CO * sizeof(float);
+  }
+  const size_t need = ((dw || dx) ? cp.col_bytes : 0) + std::max(need_dw, need_db);
+  if (ws_query) {
+    *ws_query = need;
+    return MT_OK;
+  }
+  if ((dw || dx) && cp.M > 0 && (!ws || ws_bytes < cp.col_bytes || ((uintptr_t)ws & 255)))
+    return fail(MT_ERR_WORKSPACE, "convolution: needs a 256-byte aligned workspace of "
+                                  "mt_conv2d_bwd_workspace bytes (the unfolded input)");
+  if (ws && ((uintptr_t)ws & 255)) return fail(MT_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  float* col = (float*)ws;
+  char* rest = ws ? (char*)ws + cp.col_bytes : nullptr;
+  const size_t rest_bytes = ws && ws_bytes > cp.col_bytes ? ws_bytes - cp.col_bytes : 0;
+  (void)hipGetLastError();
+  if (dw) {
+    if (cp.M > 0 && (s = hip_status(mt::conv_unfold((const float*)x->data, g, col, stream))))
+      return s;
+    gdw.p.b = col;
+    if ((s = launch_gemm(gdw, stream, rest_bytes ? rest : nullptr, rest_bytes))) return s;
+  }
+  if (db) {
+    (void)hipGetLastError();
+    float* wsp = (rest && parts > 1 && rest_bytes >= need_db) ? (float*)rest : nullptr;
+    if ((s = hip_status(mt::colsum(dy->data, false, cp.M, g.CO, g.CO, (float*)db->data, acc, wsp,
+                                   parts, stream))))
+      return s;
+  }
+  if (dx && cp.M > 0) {
+    // dU = dY Wf into the workspace (U is no longer needed), then the fold
+    GemmCall gdx{};
+    init_params(&gdx.p);
+    gdx.p.a = dy->data;
+    gdx.p.b = w->data;
+    gdx.p.c = col;
+    gdx.p.M = cp.M;
+    gdx.p.N = g.Kc;
+    gdx.p.K = g.CO;
+    gdx.p.lda = g.CO;
+    gdx.p.ldb = cp.wpitch;
+    gdx.p.ldc = g.Kcp;
+    gdx.a_kc = true;
+    gdx.b_kc = false;
+    gdx.bf16 = false;
+    gdx.vec = g.CO % 4 == 0 && aligned16(dy->data) &&
+              vec_ok_operand(w->data, g.CO, g.Kc, cp.wpitch, nullptr, 0, 4) && g.Kc % 4 == 0;
+    gdx.cfg = -1;
+    if ((s = launch_gemm(gdx, stream, nullptr, 0))) return s;
+    (void)hipGetLastError();
+    if ((s = hip_status(mt::conv_fold(col, g, (float*)dx->data, acc, stream)))) return s;
+  }
+  return MT_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -888,6 +1141,54 @@ mt_status mt_reduce_broadcast_grad_workspace(const mt_tensor* grad_out, const mt
   try {
     if (!bytes) return fail(MT_ERR_NULL, "bytes is null");
     return reduce_impl(grad_out, grad_in, 0, nullptr, 0, nullptr, bytes);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+
+mt_status mt_conv2d_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* b,
+                        const mt_tensor* y, int32_t stride_h, int32_t stride_w, int32_t pad_h,
+                        int32_t pad_w, void* ws, size_t ws_bytes, void* stream) {
+  try {
+    return conv_fwd_impl(x, w, b, y, stride_h, stride_w, pad_h, pad_w, ws, ws_bytes,
+                         (hipStream_t)stream, nullptr);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_conv2d_fwd_workspace(const mt_tensor* x, const mt_tensor* w, const mt_tensor* b,
+                                  const mt_tensor* y, int32_t stride_h, int32_t stride_w,
+                                  int32_t pad_h, int32_t pad_w, size_t* bytes) {
+  try {
+    if (!bytes) return fail(MT_ERR_NULL, "bytes is null");
+    return conv_fwd_impl(x, w, b, y, stride_h, stride_w, pad_h, pad_w, nullptr, 0, nullptr, bytes);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_conv2d_bwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* dy,
+                        const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db,
+                        int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                        uint32_t flags, void* ws, size_t ws_bytes, void* stream) {
+  try {
+    return conv_bwd_impl(x, w, dy, dx, dw, db, stride_h, stride_w, pad_h, pad_w, flags, ws,
+                         ws_bytes, (hipStream_t)stream, nullptr);
+  } catch (...) {
+    return fail(MT_ERR_INVALID, "internal error");
+  }
+}
+
+mt_status mt_conv2d_bwd_workspace(const mt_tensor* x, const mt_tensor* w, const mt_tensor* dy,
+                                  const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db,
+                                  int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                                  size_t* bytes) {
+  try {
+    if (!bytes) return fail(MT_ERR_NULL, "bytes is null");
+    return conv_bwd_impl(x, w, dy, dx, dw, db, stride_h, stride_w, pad_h, pad_w, 0, nullptr, 0,
+                         nullptr, bytes);
   } catch (...) {
     return fail(MT_ERR_INVALID, "internal error");
   }

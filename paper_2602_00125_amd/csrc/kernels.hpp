@@ -85,6 +85,23 @@ hipError_t mse(const float* p, const float* t, int64_t n, float* dp, float* loss
                int parts, hipStream_t stream);
 int mse_parts(int64_t n);
 
+// Geometry of a 2-D convolution (Sec. 3.3 Eq. (6)) in its unfolded form:
+// rows m = (n, i, j) over the output pixels, columns k over the taps.
+struct ConvGeom {
+  int32_t N, C, H, W, CO, KH, KW, sh, sw, ph, pw, HO, WO;
+  int32_t korder_uvc;  // 1: column k = (u, v, c), c fastest; 0: k = (c, u, v)
+  int32_t dx_vec;      // fold: dx channels contiguous and 16-byte aligned pixels
+  int64_t Kc, Kcp;     // columns of the unfolded matrix, and its row pitch (a multiple of 4)
+  int64_t xs[4];       // element strides of x (n, c, h, w)
+  int64_t ds[4];       // element strides of dx (n, c, h, w)
+};
+// col[m][k] = x at tap k of output pixel m (0 outside the image; columns
+// Kc .. Kcp-1 are 0). col: 16-byte aligned, N HO WO rows of pitch Kcp.
+hipError_t conv_unfold(const float* x, const ConvGeom& g, float* col, hipStream_t stream);
+// dx (+)= the fold of dcol (rows of pitch Kcp) onto the image.
+hipError_t conv_fold(const float* dcol, const ConvGeom& g, float* dx, bool accumulate,
+                     hipStream_t stream);
+
 // Up to kOptMaxTensors contiguous fp32 parameter tensors updated in one launch.
 constexpr int kOptMaxTensors = 32;
 struct OptBatch {

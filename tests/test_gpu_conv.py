@@ -1,0 +1,170 @@
+"""GPU parity of the 2-D convolution (Sec. 3.3 Eq. (6)) and its pullbacks
+against the fp64 oracle, through the C-ABI library: the unfolded input times
+the flattened weights on the matrix cores (forward, dW, dU), the unfold and
+the gather fold on the HBM side.
+
+Bar: the dense-layer bar |gpu - oracle| <= 1e-4 S + 1e-6 with S the sum of
+|terms| the oracle returns for each element (every output is a sum of
+products of inputs, as in the dense layer; the fold adds up to KH KW
+dot-product results, each within that bar, whose S add up).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2602_00125_amd import workloads as wl
+
+from helpers import assert_close, to_f64
+
+pytestmark = pytest.mark.gpu
+
+b = pytest.importorskip("paper_2602_00125_amd.binding")
+DEV = "cuda:0"
+CL = torch.channels_last
+
+# (N, C, H, W, CO, KH, KW, stride, pad, weight layout, input layout)
+CASES = [
+    (2, 3, 7, 6, 4, 3, 3, (1, 1), (1, 1), "std", "nchw"),
+    (2, 8, 9, 9, 12, 3, 3, (2, 2), (1, 1), "cl", "cl"),
+    (1, 16, 16, 16, 32, 3, 3, (1, 1), (1, 1), "cl", "cl"),
+    (2, 4, 8, 5, 8, 1, 1, (1, 1), (0, 0), "std", "cl"),
+    (1, 3, 10, 7, 5, 5, 3, (2, 1), (2, 0), "std", "nchw"),
+    (4, 32, 14, 14, 64, 3, 3, (1, 1), (1, 1), "cl", "cl"),
+    (2, 64, 28, 28, 64, 3, 3, (2, 2), (1, 1), "cl", "cl"),
+    (3, 12, 11, 13, 20, 2, 4, (3, 2), (0, 1), "std", "cl"),
+    (1, 4, 5, 5, 4, 5, 5, (1, 1), (0, 0), "cl", "nchw"),
+]
+
+
+def make(case, seed=0):
+    N, C, H, W, CO, KH, KW, st, pd, wlay, xlay = case
+    x = wl.tensor((N, C, H, W), ("normal",), seed=seed)
+    w = wl.tensor((CO, C, KH, KW), ("uniform", 1.0 / (C * KH * KW) ** 0.5), seed=seed + 1)
+    bias = wl.tensor((CO,), ("uniform", 0.5), seed=seed + 2)
+    HO, WO = oracle.conv2d_out_hw(H, W, KH, KW, st, pd)
+    dy = wl.tensor((N, CO, HO, WO), ("normal",), seed=seed + 3)
+    return x, w, bias, dy
+
+
+def to_dev(t, layout):
+    t = t.to(DEV)
+    return t.contiguous(memory_format=CL) if layout == "cl" else t.contiguous()
+
+
+def run(case, x, w, bias, dy, outputs=("dx", "dw", "db"), dx_layout="cl", accumulate=False,
+        prior=None):
+    N, C, H, W, CO, KH, KW, st, pd, wlay, xlay = case
+    HO, WO = dy.shape[2:]
+    xd, wd = to_dev(x, xlay), to_dev(w, wlay)
+    bd, dyd = bias.to(DEV), to_dev(dy, "cl")
+    y = torch.full((N, CO, HO, WO), float("nan"), device=DEV).contiguous(memory_format=CL)
+    n = b.conv2d_fwd_workspace(xd, wd, bd, y, st, pd)
+    ws = torch.empty(n // 4 + 64, device=DEV)
+    b.conv2d_fwd(xd, wd, bd, y, st, pd, workspace=ws)
+    dx = dw = db = None
+    if "dx" in outputs:
+        dx = torch.full((N, C, H, W), float("nan"), device=DEV)
+        dx = dx.contiguous(memory_format=CL) if dx_layout == "cl" else dx
+    if "dw" in outputs:
+        dw = torch.full((CO, C, KH, KW), float("nan"), device=DEV)
+        dw = dw.contiguous(memory_format=CL) if wlay == "cl" else dw
+    if "db" in outputs:
+        db = torch.full((CO,), float("nan"), device=DEV)
+    if prior is not None:
+        for t, p in zip((dx, dw, db), prior):
+            if t is not None:
+                t.copy_(p)
+    n = b.conv2d_bwd_workspace(xd, wd, dyd, dx, dw, db, st, pd)
+    ws2 = torch.empty(n // 4 + 64, device=DEV)
+    b.conv2d_bwd(xd, wd, dyd, dx, dw, db, st, pd, accumulate=accumulate, workspace=ws2)
+    torch.cuda.synchronize()
+    return y, dx, dw, db
+
+
+def check(case, x, w, bias, dy, y, dx, dw, db, prior=None):
+    st, pd = case[7], case[8]
+    X, Wt, B, dY = (to_f64(t) for t in (x, w, bias, dy))
+    Y, SY = oracle.conv2d_fwd(X, Wt, B, st, pd)
+    assert_close(to_f64(y.contiguous()), Y, SY, what="y")
+    for got, (want, S), pr, name in (
+            (dx, oracle.conv2d_bwd_dx(dY, Wt, X.shape, st, pd), 0, "dx"),
+            (dw, oracle.conv2d_bwd_dw(dY, X, Wt.shape, st, pd), 1, "dw"),
+            (db, oracle.conv2d_bwd_db(dY), 2, "db")):
+        if got is None:
+            continue
+        if prior is not None:
+            p = to_f64(prior[pr])
+            want, S = want + p, S + np.abs(p)
+        assert_close(to_f64(got.contiguous()), want, S, what=name)
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"c{i}" for i in range(len(CASES))])
+def test_conv2d_fwd_bwd(case):
+    x, w, bias, dy = make(case)
+    y, dx, dw, db = run(case, x, w, bias, dy)
+    check(case, x, w, bias, dy, y, dx, dw, db)
+
+
+def test_conv2d_optional_outputs_layouts_accumulate():
+    case = CASES[1]
+    x, w, bias, dy = make(case, seed=5)
+    y, dx, _, _ = run(case, x, w, bias, dy, outputs=("dx",), dx_layout="nchw")
+    check(case, x, w, bias, dy, y, dx, None, None)
+    _, _, dw, _ = run(case, x, w, bias, dy, outputs=("dw",))
+    check(case, x, w, bias, dy, y, None, dw, None)
+    N, C, H, W, CO, KH, KW = case[:7]
+    prior = (torch.randn(N, C, H, W, device=DEV), torch.randn(CO, C, KH, KW, device=DEV),
+             torch.randn(CO, device=DEV))
+    y, dx, dw, db = run(case, x, w, bias, dy, accumulate=True, prior=prior)
+    check(case, x, w, bias, dy, y, dx, dw, db, prior=prior)
+
+
+def test_conv2d_without_bias_and_deterministic():
+    case = CASES[5]
+    x, w, bias, dy = make(case, seed=9)
+    outs = [run(case, x, w, torch.zeros_like(bias), dy) for _ in range(2)]
+    for a, c in zip(outs[0], outs[1]):
+        assert torch.equal(a, c), "reruns must be bit-identical"
+    N, C, H, W, CO, KH, KW, st, pd, wlay, xlay = case
+    xd, wd = to_dev(x, xlay), to_dev(w, wlay)
+    y = torch.empty_like(outs[0][0])
+    n = b.conv2d_fwd_workspace(xd, wd, None, y, st, pd)
+    b.conv2d_fwd(xd, wd, None, y, st, pd, workspace=torch.empty(n // 4 + 64, device=DEV))
+    torch.cuda.synchronize()
+    assert torch.equal(y, outs[0][0]), "a zero bias and no bias give the same y"
+
+
+def test_conv2d_missing_workspace_is_an_error():
+    case = CASES[0]
+    x, w, bias, dy = make(case)
+    y = torch.empty(2, 4, 7, 6, device=DEV).contiguous(memory_format=CL)
+    with pytest.raises(b.MtError) as e:
+        b.conv2d_fwd(x.to(DEV), w.to(DEV), bias.to(DEV), y, 1, 1)
+    assert e.value.status == 7
+
+
+def test_conv2d_large_sampled():
+    """32 x 256 x 56 x 56 input, 256 3x3 filters, stride 1, padding 1: the
+    shape the bench times. Sampled y, dx, dw elements against the oracle,
+    db in full."""
+    case = (32, 256, 56, 56, 256, 3, 3, (1, 1), (1, 1), "cl", "cl")
+    x, w, bias, dy = make(case, seed=21)
+    y, dx, dw, db = run(case, x, w, bias, dy)
+    X, Wt, B, dY = (to_f64(t) for t in (x, w, bias, dy))
+    rng = np.random.default_rng(0)
+    st, pd = case[7], case[8]
+    yn = to_f64(y.contiguous())
+    f = rng.integers(0, yn.size, 3000)
+    want, S = oracle.conv2d_fwd_at(X, Wt, B, f, st, pd)
+    assert_close(yn.flat[f], want, S, what="y sampled")
+    dxn = to_f64(dx.contiguous())
+    f = rng.integers(0, dxn.size, 3000)
+    want, S = oracle.conv2d_bwd_dx_at(dY, Wt, X.shape, f, st, pd)
+    assert_close(dxn.flat[f], want, S, what="dx sampled")
+    dwn = to_f64(dw.contiguous())
+    f = rng.integers(0, dwn.size, 300)
+    want, S = oracle.conv2d_bwd_dw_at(dY, X, Wt.shape, f, st, pd)
+    assert_close(dwn.flat[f], want, S, what="dw sampled")
+    want, S = oracle.conv2d_bwd_db(dY)
+    assert_close(to_f64(db), want, S, what="db")
