@@ -315,6 +315,94 @@ def bench_mlp(args, w, inp, dev):
     print(json.dumps(out), flush=True)
 
 
+def cpu_baseline_conv(w, inp, seconds: float):
+    """Time the fp64 oracle on sampled output elements of the convolution's
+    forward, dX and dW (each a full-length sum with the |a*b| bound)."""
+    import numpy as np
+
+    import oracle
+
+    X, W, B, dY = (inp[k].double().numpy() for k in ("x", "w", "b", "dy"))
+    st, pd = w.stride, w.pad
+    rng = np.random.default_rng(0)
+    macs = done = 0
+    kc = w.C * w.KH * w.KW
+    HO, WO = w.out_hw()
+    chunk = 64
+    t0 = time.perf_counter()
+    while True:
+        oracle.conv2d_fwd_at(X, W, B, rng.integers(0, dY.size, chunk), st, pd)
+        oracle.conv2d_bwd_dx_at(dY, W, X.shape, rng.integers(0, X.size, chunk), st, pd)
+        oracle.conv2d_bwd_dw_at(dY, X, W.shape, rng.integers(0, W.size, max(1, chunk // 64)), st, pd)
+        macs += chunk * kc + chunk * w.CO * w.KH * w.KW + max(1, chunk // 64) * w.N * HO * WO
+        done += chunk
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+        if el < seconds / 8:
+            chunk *= 2
+    el = time.perf_counter() - t0
+    return {"value": 2.0 * macs / el / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"{done} random elements of y and of dx and {max(1, done // 64)} of dw (full "
+                      f"fp64 sums with the |a*b| bound) in {el:.1f} s; TFLOP/s = 2*MACs/s"}
+
+
+def bench_conv(args, w, inp, dev):
+    """Convolution step: forward (unfold + product with the bias epilogue),
+    then the backward call producing dx, dw and db (dW product on the
+    forward's unfolded input, column sum, dU product, fold)."""
+    import torch
+
+    from paper_2602_00125_amd import binding as mt
+
+    cl = torch.channels_last
+    x = inp["x"].to(dev).contiguous(memory_format=cl)
+    wt = inp["w"].to(dev).contiguous(memory_format=cl)
+    bias = inp["b"].to(dev)
+    dy = inp["dy"].to(dev).contiguous(memory_format=cl)
+    HO, WO = w.out_hw()
+    y = torch.empty(w.N, w.CO, HO, WO, device=dev).contiguous(memory_format=cl)
+    dx = torch.empty(w.N, w.C, w.H, w.W, device=dev).contiguous(memory_format=cl)
+    dw = torch.empty_like(wt)
+    db = torch.empty(w.CO, device=dev)
+    st, pd = w.stride, w.pad
+    need = max(mt.conv2d_fwd_workspace(x, wt, bias, y, st, pd),
+               mt.conv2d_bwd_workspace(x, wt, dy, dx, dw, db, st, pd))
+    ws = torch.empty(need // 4 + 64, device=dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        mt.conv2d_fwd(x, wt, bias, y, st, pd, workspace=ws)
+        if ev is not None:
+            ev[1].record()
+        # the backward finds the forward's unfolded input still in the workspace
+        mt.conv2d_bwd(x, wt, dy, dx, dw, db, st, pd, workspace=ws, reuse_unfold=True)
+        if ev is not None:
+            ev[2].record()
+
+    ms, _ = timed_steps(step, 1, args.steps, args.warmup)
+    _, per = timed_steps(step, 3, args.steps, 1)
+    per = dict(zip(["conv2d_fwd", "conv2d_bwd"], per))
+    value = w.flops() / (ms * 1e-3) / 1e12
+    out = {"metric": f"TFLOP/s for a 2-D convolution fwd+bwd (3 products) on {args.workload}",
+           "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": args.workload, "x": [w.N, w.C, w.H, w.W],
+                      "w": [w.CO, w.C, w.KH, w.KW], "stride": list(st), "pad": list(pd),
+                      "layout": "channels-last",
+                      "pct_of_mfma_peak": round(100.0 * value / FP32_MFMA_PEAK_TFLOPS, 2)},
+           "roofline": {"bound": "mfma", "kernel": "whole step (per-kernel: rocprofv3 summary)",
+                        "achieved": round(value, 3), "peak": FP32_MFMA_PEAK_TFLOPS,
+                        "unit": "TFLOP/s", "frac": round(value / FP32_MFMA_PEAK_TFLOPS, 4),
+                        "traffic": None},
+           "calls_ms": {k: round(v, 4) for k, v in per.items()}}
+    out["cpu_baseline"] = cpu_baseline_conv(w, inp, args.cpu_seconds) if args.cpu_seconds > 0 else None
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_probe:
@@ -336,6 +424,8 @@ def main():
         return bench_bmm(args, w, inp, dev)
     if isinstance(w, wl.MlpWorkload):
         return bench_mlp(args, w, inp, dev)
+    if isinstance(w, wl.ConvWorkload):
+        return bench_conv(args, w, inp, dev)
     x, wt, bias, dy = (inp[k].to(dev) for k in ("X", "W", "b", "dY"))
     M, N, K = w.M, w.N, w.K
     y = torch.empty(M, N, device=dev)

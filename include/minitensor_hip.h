@@ -81,6 +81,12 @@ typedef struct {
 #define MT_REDUCE_INTO 2u  /* mt_matmul: c may have the shape of the full result
                               summed over some batch axes (the un-broadcast shape
                               of an operand); the sum is folded into the product */
+#define MT_CONV_REUSE_UNFOLD 4u  /* mt_conv2d_bwd: the start of ws still holds the
+                              unfolded input that mt_conv2d_fwd wrote there for the
+                              same x, w, stride and padding (the forward's workspace
+                              passed again, untouched since); dw then skips the
+                              unfolding. The backward overwrites it (when dx is
+                              asked), so it serves one backward. */
 
 /* ------------------------------------------------------------------ linear
  * mt_linear_fwd: Y = X W^T + 1 b^T (Eq. (5); with b == NULL, Eq. (1)).
@@ -237,7 +243,7 @@ mt_status mt_conv2d_fwd_workspace(const mt_tensor* x, const mt_tensor* w, const 
  *   dy [N, CO, Ho, Wo] channels-last contiguous; dx [N, C, H, W] contiguous,
  *   channels-last or [N][C][H][W]; dw the shape of w with its taps in w's
  *   order; db [CO]. x and w are needed for their shapes (and x's data for
- *   dw, w's data for dx). flags: MT_ACCUMULATE. The input gradient is a
+ *   dw, w's data for dx). flags: MT_ACCUMULATE, MT_CONV_REUSE_UNFOLD. The input gradient is a
  *   gather over the taps that read each element: no atomics, deterministic.
  */
 mt_status mt_conv2d_bwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* dy,

@@ -21,7 +21,7 @@ lib = ctypes.CDLL(LIB_PATH)
 
 MAX_DIMS = 8
 F32, BF16 = 0, 1
-ACCUMULATE, REDUCE_INTO = 1, 2
+ACCUMULATE, REDUCE_INTO, CONV_REUSE_UNFOLD = 1, 2, 4
 STATUS = {0: "MT_OK", 1: "MT_ERR_NULL", 2: "MT_ERR_NDIM", 3: "MT_ERR_SHAPE", 4: "MT_ERR_DTYPE",
           5: "MT_ERR_LAYOUT", 6: "MT_ERR_ALIAS", 7: "MT_ERR_WORKSPACE", 8: "MT_ERR_HIP",
           9: "MT_ERR_INVALID"}
@@ -302,13 +302,15 @@ def conv2d_bwd_workspace(x, w, dy, dx=None, dw=None, db=None, stride=1, padding=
 
 
 def conv2d_bwd(x, w, dy, dx=None, dw=None, db=None, stride=1, padding=0, accumulate=False,
-               workspace=None, stream=None) -> None:
-    """Pullbacks of conv2d: dx, dw, db (None skips one)."""
+               workspace=None, reuse_unfold=False, stream=None) -> None:
+    """Pullbacks of conv2d: dx, dw, db (None skips one). reuse_unfold: the
+    workspace still holds the forward's unfolded input."""
     st, pd = _pair(stride), _pair(padding)
     ds = [desc(t) for t in (x, w, dy, dx, dw, db)]
     ptr, nbytes = _ws(workspace)
-    _check(lib.mt_conv2d_bwd(*[_ref(d) for d in ds], *st, *pd, ACCUMULATE if accumulate else 0,
-                             ptr, nbytes, _stream(stream)), "mt_conv2d_bwd")
+    flags = (ACCUMULATE if accumulate else 0) | (CONV_REUSE_UNFOLD if reuse_unfold else 0)
+    _check(lib.mt_conv2d_bwd(*[_ref(d) for d in ds], *st, *pd, flags, ptr, nbytes,
+                             _stream(stream)), "mt_conv2d_bwd")
 
 
 def _shape_call(fn, a, b, where):

@@ -95,8 +95,12 @@ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // SIMD each), which hides one block's barrier behind the other's matrix-core
 // work (measured faster than 256x256 on 8192^3). Smaller problems take
 // 128x128 when split-K can fill the chip, else 64x64.
+// K-stages of the 256x256 DMA tile per split-K run below which a run is too
+// short to amortise its prologue and epilogue
+constexpr int64_t kDmaMinRunStages = 32;
+
 int choose_cfg(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_split, bool bf16,
-               bool a_kc, bool b_kc) {
+               bool a_kc, bool b_kc, bool vec, int64_t K, int64_t red) {
   if (g_force_cfg >= 0) return g_force_cfg;
   auto tiles = [&](int64_t bm, int64_t bn) { return cdiv(M, bm) * cdiv(N, bn) * batch; };
   // Large products (measured on 8192^3 fp32 and 16384x8192x8192 bf16, all
@@ -104,6 +108,15 @@ int choose_cfg(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_spl
   // two-stage LDS ring, one block of 8 waves per CU, once there are enough
   // tiles to fill every CU.
   if (tiles(256, 256) >= 256) return mt::kCfgDma256x256;
+  // A few such tiles over a long contraction (e.g. the weight gradient of a
+  // convolution, K = every output pixel): the same tile, its K-stages split
+  // into runs that fill the chip once, each run at least kDmaMinRunStages long
+  if (can_split && vec) {
+    const int64_t t = tiles(256, 256);
+    const int64_t dma_stages = cdiv(K, bf16 ? 64 : 32) * red;
+    if (t > 0 && 256 / t >= 2 && dma_stages / (256 / t) >= kDmaMinRunStages)
+      return mt::kCfgDma256x256;
+  }
   (void)a_kc;
   (void)b_kc;
   (void)bf16;
@@ -117,8 +130,14 @@ int choose_cfg(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_spl
 // Split-K runs for a grid of `blocks` tiles over `stages` K-stages: below
 // two blocks per CU, aim for ~512 blocks in all, with at least 8 stages per
 // run and at most 16 runs.
-int choose_splits(int64_t blocks, int64_t stages) {
+int choose_splits(int64_t blocks, int64_t stages, int cfg) {
   if (g_force_splits > 0) return (int)std::min<int64_t>(g_force_splits, std::max<int64_t>(stages, 1));
+  if (cfg == mt::kCfgDma256x256) {
+    // one block per CU: runs that together fill the 256 CUs once
+    if (blocks >= 256) return 1;
+    int64_t s = std::min<int64_t>(256 / blocks, stages / kDmaMinRunStages);
+    return s < 1 ? 1 : (int)s;
+  }
   if (blocks >= 512) return 1;
   int64_t s = cdiv(512, blocks);
   s = std::min<int64_t>(s, stages / 8);
@@ -180,7 +199,8 @@ size_t plan_gemm(GemmCall& g, bool may_split) {
   if (g_force_vec1) g.vec = false;
   const int64_t stages_guess = cdiv(p.K, g.bf16 ? 32 : 16) * p.red_count;
   if (g.cfg < 0)
-    g.cfg = choose_cfg(p.M, p.N, p.keep_count, stages_guess, may_split, g.bf16, g.a_kc, g.b_kc);
+    g.cfg = choose_cfg(p.M, p.N, p.keep_count, stages_guess, may_split, g.bf16, g.a_kc, g.b_kc,
+                       g.vec, p.K, p.red_count);
   // the element-load kernels keep their staging registers within budget up to 128x128
   if (!g.vec && g.cfg != mt::kCfg64x64) g.cfg = mt::kCfg128x128;
   const int64_t stages = cdiv(p.K, mt::gemm_tile_k(g.cfg, g.bf16)) * p.red_count;
@@ -191,7 +211,7 @@ size_t plan_gemm(GemmCall& g, bool may_split) {
   if (!may_split || p.M == 0 || p.N == 0 || p.keep_count == 0 || stages == 0) return 0;
   const int64_t blocks = cdiv(p.M, mt::gemm_tile_m(g.cfg)) * cdiv(p.N, mt::gemm_tile_n(g.cfg)) *
                          p.keep_count;
-  const int want = choose_splits(blocks, stages);
+  const int want = choose_splits(blocks, stages, g.cfg);
   if (want <= 1) return 0;
   const int64_t per = cdiv(stages, want);
   const int64_t splits = cdiv(stages, per);
@@ -840,7 +860,8 @@ mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
                         const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db, int32_t sh,
                         int32_t sw, int32_t ph, int32_t pw, uint32_t flags, void* ws,
                         size_t ws_bytes, hipStream_t stream, size_t* ws_query) {
-  if (flags & ~MT_ACCUMULATE) return fail(MT_ERR_INVALID, "mt_conv2d_bwd: unknown flags");
+  if (flags & ~(MT_ACCUMULATE | MT_CONV_REUSE_UNFOLD))
+    return fail(MT_ERR_INVALID, "mt_conv2d_bwd: unknown flags");
   ConvPlan cp;
   mt_status s = conv_plan(x, w, sh, sw, ph, pw, &cp);
   if (s) return s;
@@ -924,7 +945,9 @@ mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
   const size_t rest_bytes = ws && ws_bytes > cp.col_bytes ? ws_bytes - cp.col_bytes : 0;
   (void)hipGetLastError();
   if (dw) {
-    if (cp.M > 0 && (s = hip_status(mt::conv_unfold((const float*)x->data, g, col, stream))))
+    // MT_CONV_REUSE_UNFOLD: the forward left the unfolded input at the start of ws
+    if (cp.M > 0 && !(flags & MT_CONV_REUSE_UNFOLD) &&
+        (s = hip_status(mt::conv_unfold((const float*)x->data, g, col, stream))))
       return s;
     gdw.p.b = col;
     if ((s = launch_gemm(gdw, stream, rest_bytes ? rest : nullptr, rest_bytes))) return s;

@@ -14,9 +14,10 @@
 //   dx[n][c][h][x] = sum over taps (u, v) with h = i sh + u - ph, x = j sw + v - pw
 //                    (i, j inside the output) of dU[(n, i, j)][k(c, u, v)].
 //
-// unfold_kernel: one block row per output pixel m (decoded once per block),
-// each lane writes 4 consecutive k of U with one 16-byte store; channels-last
-// x with k = (u, v, c) reads 4 channels with one 16-byte load.
+// unfold_kernel: a block per 8 output pixels (decoded once per block); a
+// lane decodes the taps of its groups of 4 columns once and writes them in
+// all 8 rows with 16-byte stores; channels-last x with k = (u, v, c) reads 4
+// channels with one 16-byte load.
 // fold_kernel: a lane per input element (or 4 channels of one), summing the
 // taps in a fixed (u, v) order: a gather, so no atomics and bit-identical
 // reruns.
@@ -44,40 +45,67 @@ __device__ __forceinline__ void decode_k(const ConvGeom& g, int64_t k, int& c, i
   }
 }
 
+// Block b fills rows m = b R .. b R + R - 1 of the unfolded matrix. Each
+// lane takes the column groups k4 = tid, tid + 256, ... (4 columns, one
+// 16-byte store each), decodes their tap once, and writes that group in all
+// R rows; the rows' pixel origins are decoded once per block (uniform).
 // FAST: k = (u, v, c), x channels contiguous and 16-byte aligned, C % 4 == 0.
+constexpr int kUnfoldRows = 8;
+
 template <bool FAST>
-__global__ __launch_bounds__(256) void unfold_kernel(const float* x, const ConvGeom g, float* col) {
-  const int64_t m = blockIdx.x;
-  const int64_t k0 = ((int64_t)blockIdx.y * 256 + threadIdx.x) * 4;
-  if (k0 >= g.Kcp) return;
-  const int j = (int)(m % g.WO);
-  const int64_t t = m / g.WO;
-  const int i = (int)(t % g.HO);
-  const int64_t n = t / g.HO;
-  const float* xn = x + n * g.xs[0];
-  const int hb = i * g.sh - g.ph, wb = j * g.sw - g.pw;
-  f32x4 out = {0.f, 0.f, 0.f, 0.f};
-  if (FAST) {
-    if (k0 < g.Kc) {
-      int c, u, v;
-      decode_k(g, k0, c, u, v);
-      const int h = hb + u, w = wb + v;
-      if (h >= 0 && h < g.H && w >= 0 && w < g.W)
-        out = *(const f32x4*)(xn + (int64_t)h * g.xs[2] + (int64_t)w * g.xs[3] + c);
-    }
-  } else {
+__global__ __launch_bounds__(256) void unfold_kernel(const float* x, const ConvGeom g, float* col,
+                                                     int64_t M) {
+  const int64_t m0 = (int64_t)blockIdx.x * kUnfoldRows;
+  const int64_t Kcp4 = g.Kcp / 4;
+  int64_t nb[kUnfoldRows];  // x offset of image n
+  int hb[kUnfoldRows], wb[kUnfoldRows];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int64_t k = k0 + e;
-      if (k >= g.Kc) break;
-      int c, u, v;
-      decode_k(g, k, c, u, v);
-      const int h = hb + u, w = wb + v;
-      if (h >= 0 && h < g.H && w >= 0 && w < g.W)
-        out[e] = xn[c * g.xs[1] + (int64_t)h * g.xs[2] + (int64_t)w * g.xs[3]];
+  for (int r = 0; r < kUnfoldRows; ++r) {
+    const int64_t m = m0 + r < M ? m0 + r : M - 1;
+    const int j = (int)(m % g.WO);
+    const int64_t t = m / g.WO;
+    hb[r] = (int)(t % g.HO) * g.sh - g.ph;
+    wb[r] = j * g.sw - g.pw;
+    nb[r] = (t / g.HO) * g.xs[0];
+  }
+  const int rows = M - m0 < kUnfoldRows ? (int)(M - m0) : kUnfoldRows;
+  for (int64_t k4 = threadIdx.x; k4 < Kcp4; k4 += 256) {
+    const int64_t k0 = 4 * k4;
+    if (FAST) {
+      int c = 0, u = 0, v = 0;
+      const bool live = k0 < g.Kc;
+      if (live) decode_k(g, k0, c, u, v);
+      f32x4 vals[kUnfoldRows];
+#pragma unroll
+      for (int r = 0; r < kUnfoldRows; ++r) {
+        const int h = hb[r] + u, w = wb[r] + v;
+        vals[r] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (live && r < rows && h >= 0 && h < g.H && w >= 0 && w < g.W)
+          vals[r] = *(const f32x4*)(x + nb[r] + (int64_t)h * g.xs[2] + (int64_t)w * g.xs[3] + c);
+      }
+#pragma unroll
+      for (int r = 0; r < kUnfoldRows; ++r)
+        if (r < rows) *(f32x4*)(col + (m0 + r) * g.Kcp + k0) = vals[r];
+    } else {
+      int cs[4], us[4], vs[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        cs[e] = -1;
+        if (k0 + e < g.Kc) decode_k(g, k0 + e, cs[e], us[e], vs[e]);
+      }
+      for (int r = 0; r < rows; ++r) {
+        f32x4 out = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (cs[e] < 0) continue;
+          const int h = hb[r] + us[e], w = wb[r] + vs[e];
+          if (h >= 0 && h < g.H && w >= 0 && w < g.W)
+            out[e] = x[nb[r] + cs[e] * g.xs[1] + (int64_t)h * g.xs[2] + (int64_t)w * g.xs[3]];
+        }
+        *(f32x4*)(col + (m0 + r) * g.Kcp + k0) = out;
+      }
     }
   }
-  *(f32x4*)(col + m * g.Kcp + k0) = out;
 }
 
 // Sum over the taps reading input element (n, c, h, w); FAST: 4 channels at
@@ -140,16 +168,16 @@ __global__ __launch_bounds__(256) void fold_kernel(const float* dcol, const Conv
 hipError_t conv_unfold(const float* x, const ConvGeom& g, float* col, hipStream_t stream) {
   const int64_t M = (int64_t)g.N * g.HO * g.WO;
   if (M <= 0 || g.Kcp <= 0) return hipSuccess;
-  const int64_t ky = (g.Kcp + 1023) / 1024;
-  if (M > 0x7fffffff || ky > 65535) return hipErrorInvalidConfiguration;
+  const int64_t blocks = (M + kUnfoldRows - 1) / kUnfoldRows;
+  if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   const bool fast = g.korder_uvc && g.xs[1] == 1 && g.C % 4 == 0 && (uintptr_t)x % 16 == 0 &&
                     g.xs[0] % 4 == 0 && g.xs[2] % 4 == 0 && g.xs[3] % 4 == 0;
   if (fast)
-    hipLaunchKernelGGL(unfold_kernel<true>, dim3((unsigned)M, (unsigned)ky), dim3(256), 0, stream, x,
-                       g, col);
+    hipLaunchKernelGGL(unfold_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream, x, g, col,
+                       M);
   else
-    hipLaunchKernelGGL(unfold_kernel<false>, dim3((unsigned)M, (unsigned)ky), dim3(256), 0, stream,
-                       x, g, col);
+    hipLaunchKernelGGL(unfold_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream, x, g, col,
+                       M);
   return hipGetLastError();
 }
 

@@ -120,6 +120,42 @@ class MlpWorkload:
                 for n in ("X", "W1", "b1", "W2", "b2", "T")}
 
 
+@dataclass
+class ConvWorkload:
+    """2-D convolution forward and backward: x[N,C,H,W], w[CO,C,KH,KW], b[CO],
+    dy[N,CO,Ho,Wo], fp32, stride and zero padding; drawn in that order."""
+    name: str
+    N: int
+    C: int
+    H: int
+    W: int
+    CO: int
+    KH: int
+    KW: int
+    stride: tuple = (1, 1)
+    pad: tuple = (0, 0)
+    dist: dict = field(default_factory=dict)
+    seed: int = 0
+
+    def out_hw(self):
+        return ((self.H + 2 * self.pad[0] - self.KH) // self.stride[0] + 1,
+                (self.W + 2 * self.pad[1] - self.KW) // self.stride[1] + 1)
+
+    def flops(self) -> float:
+        """Multiply-adds of the three products (forward, dW, dX), 2 flops each."""
+        HO, WO = self.out_hw()
+        return 3 * 2.0 * self.N * HO * WO * self.CO * self.C * self.KH * self.KW
+
+    def make(self, seed: int | None = None) -> dict:
+        g = torch.Generator("cpu")
+        g.manual_seed(self.seed if seed is None else seed)
+        HO, WO = self.out_hw()
+        shapes = {"x": (self.N, self.C, self.H, self.W), "w": (self.CO, self.C, self.KH, self.KW),
+                  "b": (self.CO,), "dy": (self.N, self.CO, HO, WO)}
+        return {n: _draw(g, shapes[n], self.dist.get(n, ("uniform", 1.0)))
+                for n in ("x", "w", "b", "dy")}
+
+
 def _u(a):
     return ("uniform", a)
 
@@ -150,9 +186,17 @@ MLP2_8192x8192x8192x8192_F32_GELU = MlpWorkload(
     dist={"X": N01, "W1": _u(1 / math.sqrt(8192)), "b1": _u(1 / math.sqrt(8192)),
           "W2": _u(1 / math.sqrt(8192)), "b2": _u(1 / math.sqrt(8192)), "T": N01})
 
+# A 3x3 convolution layer of the size found mid-way through image classifiers:
+# 32 images of 256 channels at 56 x 56, 256 filters, stride 1, padding 1.
+CONV2D_32x256x56x56_256x3x3_F32 = ConvWorkload(
+    "conv2d_32x256x56x56_256x3x3_s1p1_f32", N=32, C=256, H=56, W=56, CO=256, KH=3, KW=3,
+    stride=(1, 1), pad=(1, 1),
+    dist={"x": N01, "w": _u(1 / math.sqrt(256 * 9)), "b": _u(1 / math.sqrt(256 * 9)), "dy": N01})
+
 WORKLOADS = {w.name: w for w in (LINEAR_64x32x128_F32, LINEAR_4096x1024x1024_F32,
                                  LINEAR_8192x8192x8192_F32, BMM_BCAST_16x1x509x257_1x8x257x383_F32,
-                                 LINEAR_16384x8192x8192_BF16, MLP2_8192x8192x8192x8192_F32_GELU)}
+                                 LINEAR_16384x8192x8192_BF16, MLP2_8192x8192x8192x8192_F32_GELU,
+                                 CONV2D_32x256x56x56_256x3x3_F32)}
 
 
 def linear(M, N, K, dtype="f32", dist=None, seed=0, name=None) -> LinearWorkload:

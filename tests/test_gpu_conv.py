@@ -168,3 +168,22 @@ def test_conv2d_large_sampled():
     assert_close(dwn.flat[f], want, S, what="dw sampled")
     want, S = oracle.conv2d_bwd_db(dY)
     assert_close(to_f64(db), want, S, what="db")
+
+
+def test_conv2d_backward_reuses_the_forward_unfold():
+    case = CASES[6]
+    x, w, bias, dy = make(case, seed=13)
+    N, C, H, W, CO, KH, KW, st, pd, wlay, xlay = case
+    HO, WO = dy.shape[2:]
+    xd, wd, bd, dyd = to_dev(x, xlay), to_dev(w, wlay), bias.to(DEV), to_dev(dy, "cl")
+    y = torch.empty(N, CO, HO, WO, device=DEV).contiguous(memory_format=CL)
+    dx = torch.empty(N, C, H, W, device=DEV).contiguous(memory_format=CL)
+    dw = torch.empty_like(wd)
+    db = torch.empty(CO, device=DEV)
+    need = max(b.conv2d_fwd_workspace(xd, wd, bd, y, st, pd),
+               b.conv2d_bwd_workspace(xd, wd, dyd, dx, dw, db, st, pd))
+    ws = torch.empty(need // 4 + 64, device=DEV)
+    b.conv2d_fwd(xd, wd, bd, y, st, pd, workspace=ws)
+    b.conv2d_bwd(xd, wd, dyd, dx, dw, db, st, pd, workspace=ws, reuse_unfold=True)
+    torch.cuda.synchronize()
+    check(case, x, w, bias, dy, y, dx, dw, db)

@@ -133,3 +133,33 @@ def test_dma_tile_k_rotation_settings(krot, dtype):
     r, c = sample_positions(N, K, 2000, seed=krot + 7)
     want, S = oracle.linear_bwd_dw_at(dY, X, r, c)
     assert_close(to_f64(outs[0][1])[r, c], want, S, what="dW")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_few_tiles_long_contraction_dma_split(dtype):
+    """dW of a 65536-row layer with 512 x 512 weights: four 256x256 output
+    tiles over 65536 summed rows run on the DMA tile split into 64 runs (one
+    wave of 256 blocks) with a fixed-order second pass. Sampled against the
+    oracle; reruns bit-identical; the same without workspace (unsplit)."""
+    M, N, K = 65536, 512, 512
+    inp = wl.linear(M, N, K, dtype=dtype, seed=4, dist={"X": ("normal",), "dY": ("normal",)}).make()
+    x, w, dy = (inp[k].to(DEV) for k in ("X", "W", "dY"))
+    outs = []
+    for use_ws in (True, True, False):
+        dw = torch.full((N, K), float("nan"), device=DEV)
+        ws = None
+        if use_ws:
+            n = b.linear_bwd_workspace(x, w, dy, None, dw, None)
+            # fp32: 2048 K-stages of 32 -> 64 runs of 32 on the DMA tile; bf16
+            # (stages of 64) stays below the run length and splits on 128x128
+            assert n >= (64 if dtype == "f32" else 2) * N * K * 4, n
+            ws = torch.empty(n // 4 + 64, device=DEV)
+        b.linear_bwd(x, w, dy, None, dw, None, workspace=ws)
+        torch.cuda.synchronize()
+        outs.append(dw)
+    assert torch.equal(outs[0], outs[1])
+    X, dY = to_f64(inp["X"]), to_f64(inp["dY"])
+    r, c = sample_positions(N, K, 1500, seed=3)
+    want, S = oracle.linear_bwd_dw_at(dY, X, r, c)
+    for o, what in ((outs[0], "split"), (outs[2], "unsplit")):
+        assert_close(to_f64(o)[r, c], want, S, what=f"dW ({what})")
