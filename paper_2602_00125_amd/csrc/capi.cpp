@@ -99,9 +99,30 @@ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // short to amortise its prologue and epilogue
 constexpr int64_t kDmaMinRunStages = 32;
 
+int choose_cfg_aligned(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_split,
+                       bool bf16, bool a_kc, bool b_kc, bool vec, int64_t K, int64_t red);
+
+// Tile choice. fp32 products whose operands or output lack 16-byte aligned
+// rows run on the DMA tiles with 4-byte lanes (or 128x128 register-staged
+// element loads); below ~4 waves of 256x256 tiles the tile that wastes least
+// on the matrix edges wins (measured on the 16x1x509x257 @ 1x8x257x383
+// products: 256x128 for 509 x 383 and 509 x 257 outputs, 128x128 for 257 x 383).
 int choose_cfg(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_split, bool bf16,
                bool a_kc, bool b_kc, bool vec, int64_t K, int64_t red) {
   if (g_force_cfg >= 0) return g_force_cfg;
+  const int c = choose_cfg_aligned(M, N, batch, stages, can_split, bf16, a_kc, b_kc, vec, K, red);
+  if (vec || bf16 || c == mt::kCfg64x64) return c;
+  if (cdiv(M, 256) * cdiv(N, 256) * batch >= 1024) return mt::kCfgDma256x256;
+  auto used = [&](int64_t bm, int64_t bn) {
+    return (double)(M * N) / (double)(cdiv(M, bm) * bm * cdiv(N, bn) * bn);
+  };
+  const double u8 = used(256, 128), u9 = used(128, 256), u3 = used(128, 128);
+  if (std::max(u8, u9) >= 0.9 * u3) return u8 >= u9 ? mt::kCfgDma256x128 : mt::kCfgDma128x256;
+  return mt::kCfg128x128;
+}
+
+int choose_cfg_aligned(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_split,
+                       bool bf16, bool a_kc, bool b_kc, bool vec, int64_t K, int64_t red) {
   auto tiles = [&](int64_t bm, int64_t bn) { return cdiv(M, bm) * cdiv(N, bn) * batch; };
   // Large products (measured on 8192^3 fp32 and 16384x8192x8192 bf16, all
   // three layouts): the 256x256 tile whose operands stream straight into a
@@ -111,7 +132,7 @@ int choose_cfg(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_spl
   // A few such tiles over a long contraction (e.g. the weight gradient of a
   // convolution, K = every output pixel): the same tile, its K-stages split
   // into runs that fill the chip once, each run at least kDmaMinRunStages long
-  if (can_split && vec) {
+  if (can_split && (vec || !bf16)) {
     const int64_t t = tiles(256, 256);
     const int64_t dma_stages = cdiv(K, bf16 ? 64 : 32) * red;
     if (t > 0 && 256 / t >= 2 && dma_stages / (256 / t) >= kDmaMinRunStages)
@@ -201,8 +222,19 @@ size_t plan_gemm(GemmCall& g, bool may_split) {
   if (g.cfg < 0)
     g.cfg = choose_cfg(p.M, p.N, p.keep_count, stages_guess, may_split, g.bf16, g.a_kc, g.b_kc,
                        g.vec, p.K, p.red_count);
-  // the element-load kernels keep their staging registers within budget up to 128x128
-  if (!g.vec && g.cfg != mt::kCfg64x64) g.cfg = mt::kCfg128x128;
+  // operands or output without 16-byte aligned rows: fp32 keeps the DMA tiles
+  // (4-byte lanes, element stores) and maps the register-staged tiles above
+  // 128x128 to them; the element-load register-staged kernels stop at 128x128
+  if (!g.vec) {
+    const bool dma = g.cfg == mt::kCfgDma256x256 || g.cfg == mt::kCfgDma256x128 ||
+                     g.cfg == mt::kCfgDma128x256;
+    if (!g.bf16 && (dma || g.cfg == mt::kCfg256x128 || g.cfg == mt::kCfg128x256)) {
+      if (g.cfg == mt::kCfg256x128) g.cfg = mt::kCfgDma256x128;
+      if (g.cfg == mt::kCfg128x256) g.cfg = mt::kCfgDma128x256;
+    } else if (g.cfg != mt::kCfg64x64) {
+      g.cfg = mt::kCfg128x128;
+    }
+  }
   const int64_t stages = cdiv(p.K, mt::gemm_tile_k(g.cfg, g.bf16)) * p.red_count;
   p.splits = 1;
   p.stages_per_split = stages > 0 ? stages : 1;

@@ -61,6 +61,15 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, u
                        : "memory", "m0");
 }
 
+// The 4-byte form, for operands whose rows are not 16-byte aligned (odd
+// pitches): lane i's 4 bytes land at lds_byte + 4 i.
+__device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds_byte) {
+  __asm__ __volatile__("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+                       :
+                       : "s"(lds_byte), "v"(voff), "s"(r)
+                       : "memory", "m0");
+}
+
 // The same address in every lane, taken from lane 0: the compiler may keep a
 // wave-uniform 64-bit offset in vector registers (after a 64-bit division),
 // and the LDS-DMA load takes its buffer descriptor in scalar registers only.
@@ -117,28 +126,46 @@ struct DmaTile {
   }
 };
 
-// Per-lane DMA plan of one operand: the wave issues JB instructions per stage.
-template <int ES, bool KC, int BMN, int BK, int NW>
+// Per-lane DMA plan of one operand: the wave issues JB instructions per
+// stage, each moving 64 lanes x LANE bytes (16: one chunk a lane; 4: one
+// element a lane, for operands without 16-byte aligned rows).
+template <int ES, bool KC, int BMN, int BK, int NW, int LANE = 16>
 struct DmaLoader {
   using T = DmaTile<ES, KC, BMN, BK>;
-  static constexpr int JB = T::BLOCKS / NW;
-  static_assert(T::BLOCKS % NW == 0, "blocks split evenly over the waves");
+  static_assert(LANE == 16 || LANE == 4, "16- or 4-byte lanes");
+  static constexpr int IB = 64 * LANE;  // bytes per instruction
+  static constexpr int JB = T::BYTES / IB / NW;
+  static_assert(T::BYTES % (IB * NW) == 0, "instructions split evenly over the waves");
   // byte offset of the lane's chunk from the stage's tile origin in global
   // memory, or kOOB (reads zero) where its m / n lies past the matrix edge
   uint32_t off[JB];
-  int kx[JB];  // the chunk's k within the stage (its column if K-contiguous, else its row)
+  // the chunk's k within the stage (its column if K-contiguous, else its row);
+  // with 4-byte lanes (4x the instructions) packed four to a register (k < 256)
+  static constexpr int KXN = LANE == 16 ? JB : (JB + 3) / 4;
+  uint32_t kx[KXN];
+  __device__ __forceinline__ int kx_of(int j) const {
+    if constexpr (LANE == 16) return (int)kx[j];
+    else return (int)((kx[j >> 2] >> (8 * (j & 3))) & 0xffu);
+  }
 
   // mn_left: rows of A (columns of B) from the block's tile origin on
   __device__ __forceinline__ void init(int wave, int lane, int64_t ld, int64_t mn_left) {
 #pragma unroll
     for (int j = 0; j < JB; ++j) {
       const int b = wave + NW * j;
-      const int byte = 1024 * b + 16 * lane;
+      const int byte = IB * b + LANE * lane;
       const int r = byte / T::RB;
       const int pchunk = (byte % T::RB) / 16;
-      const int c = (pchunk ^ T::swz(r)) * T::EPC;
+      const int c = (pchunk ^ T::swz(r)) * T::EPC + (byte % 16) / ES;
       const int mn = KC ? r : c;
-      kx[j] = KC ? c : r;
+      const uint32_t k_in_stage = (uint32_t)(KC ? c : r);
+      if constexpr (LANE == 16) {
+        kx[j] = k_in_stage;
+      } else {
+        static_assert(BK <= 256, "packed k fits 8 bits");
+        if ((j & 3) == 0) kx[j >> 2] = 0;
+        kx[j >> 2] |= k_in_stage << (8 * (j & 3));
+      }
       off[j] = mn < mn_left ? (uint32_t)(((int64_t)r * ld + c) * ES) : kOOB;
     }
   }
@@ -168,8 +195,9 @@ struct DmaLoader {
   // the MFMAs cost matrix throughput).
   template <bool KTAIL>
   __device__ __forceinline__ void issue_one(const Plan& q, int j, int wave) const {
-    const uint32_t o = KTAIL ? (kx[j] < q.kl ? off[j] : kOOB) : off[j];
-    dma16(q.r, o, q.lds0 + 1024 * (wave + NW * j));
+    const uint32_t o = KTAIL ? (kx_of(j) < q.kl ? off[j] : kOOB) : off[j];
+    if constexpr (LANE == 16) dma16(q.r, o, q.lds0 + IB * (wave + NW * j));
+    else dma4(q.r, o, q.lds0 + IB * (wave + NW * j));
   }
 };
 
@@ -277,7 +305,7 @@ struct DmaMma<__bf16, A_KC, B_KC, TM, TN, BK, BM, BN> {
 
 template <typename T, bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int WGN, int NS,
           int DMA_G0, int DMA_GS, bool KTAIL,
-          int WAVES_PER_EU, bool EPI = false>
+          int WAVES_PER_EU, bool EPI = false, int DMA_LANE = 16, bool VEC_C = true>
 __global__ __launch_bounds__(WGM * WGN * 64)
 __attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
 void gemm_dma_kernel(const GemmParams p) {
@@ -286,8 +314,8 @@ void gemm_dma_kernel(const GemmParams p) {
   constexpr int WTM = BM / WGM, WTN = BN / WGN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
   static_assert(NS >= 2 && NS <= 5, "a ring of two to five stages");
-  using LA = DmaLoader<ES, A_KC, BM, BK, NW>;
-  using LB = DmaLoader<ES, B_KC, BN, BK, NW>;
+  using LA = DmaLoader<ES, A_KC, BM, BK, NW, DMA_LANE>;
+  using LB = DmaLoader<ES, B_KC, BN, BK, NW, DMA_LANE>;
   constexpr int A_BYTES = LA::T::BYTES, B_BYTES = LB::T::BYTES;
   constexpr int STAGE = A_BYTES + B_BYTES;
   constexpr int L = LA::JB + LB::JB;  // DMA instructions per wave per stage
@@ -489,6 +517,51 @@ void gemm_dma_kernel(const GemmParams p) {
   float* C = to_partial ? p.partial + (int64_t)split * p.partial_stride + batch * p.M * p.N
                         : p.c + c_off;
   const int64_t ldc = to_partial ? p.N : p.ldc;
+  if constexpr (!VEC_C) {
+    // Rows of C not 16-byte aligned (odd pitch or N): each wave stages 32
+    // rows of its tile at a time in its own slice of the (now idle) ring,
+    // then writes them back a row at a time, 64 lanes on 64 consecutive
+    // columns: one contiguous 256-byte store per row segment instead of
+    // scattered 4-byte stores. Row pitch WTN + 4 floats offsets consecutive
+    // rows by 16 bytes in the LDS banks.
+    constexpr int SP = WTN + 4;
+    static_assert(NW * 32 * SP * 4 <= NS * STAGE, "staging fits in the ring");
+    __syncthreads();  // every wave has finished reading the ring
+    float* stg = (float*)(lds + wave * 32 * SP * 4);
+    const int64_t mb = m0 + wm * WTM, nb = n0 + wn * WTN;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int q = 0; q < TN; ++q)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          *(f32x4*)&stg[l32 * SP + q * 32 + 8 * g + 4 * h] =
+              f32x4{acc[i][q][4 * g + 0], acc[i][q][4 * g + 1], acc[i][q][4 * g + 2],
+                    acc[i][q][4 * g + 3]};
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes done
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll 4
+      for (int r = 0; r < 32; ++r) {
+        const int64_t m = mb + i * 32 + r;
+        if (m >= p.M) break;
+        float* crow = C + m * ldc;
+#pragma unroll
+        for (int cb = 0; cb < WTN; cb += 64) {
+          const int64_t n = nb + cb + lane;
+          if (n >= p.N) continue;
+          float x = stg[r * SP + cb + lane];
+          if (!to_partial) {
+            if (p.bias) x += p.bias[n];
+            if (p.accumulate) x += crow[n];
+          }
+          crow[n] = x;
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the next slab overwrites
+      __builtin_amdgcn_wave_barrier();
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     const int64_t m = m0 + wm * WTM + i * 32 + l32;
@@ -499,6 +572,20 @@ void gemm_dma_kernel(const GemmParams p) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int64_t n = n0 + wn * WTN + q * 32 + 8 * g + 4 * h;
+        if constexpr (!VEC_C) {
+          // rows of C not 16-byte aligned (odd pitch or N): element stores
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (n + e >= p.N) continue;
+            float x = acc[i][q][4 * g + e];
+            if (!to_partial) {
+              if (p.bias) x += p.bias[n + e];
+              if (p.accumulate) x += crow[n + e];
+            }
+            crow[n + e] = x;
+          }
+          continue;
+        }
         if (n >= p.N) continue;
         f32x4 v = {acc[i][q][4 * g + 0], acc[i][q][4 * g + 1], acc[i][q][4 * g + 2],
                    acc[i][q][4 * g + 3]};

@@ -21,7 +21,7 @@ static hipError_t launch_f32(const GemmParams& p, hipStream_t stream) {
 }
 
 template <bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int WGN, int NS, int WPE,
-          bool EPI = false>
+          bool EPI = false, int LANE = 16, bool VEC_C = true>
 static hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
   GemmParams q = p;
   q.tiles_m = (int32_t)((p.M + BM - 1) / BM);
@@ -31,10 +31,10 @@ static hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   // the per-load K-tail test only where K is not a whole number of stages
   if (p.K % BK != 0)
-    hipLaunchKernelGGL((gemm::gemm_dma_kernel<float, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 1, 1, true, WPE, EPI>),
+    hipLaunchKernelGGL((gemm::gemm_dma_kernel<float, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 1, 1, true, WPE, EPI, LANE, VEC_C>),
                        dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
   else
-    hipLaunchKernelGGL((gemm::gemm_dma_kernel<float, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 1, 1, false, WPE, EPI>),
+    hipLaunchKernelGGL((gemm::gemm_dma_kernel<float, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 1, 1, false, WPE, EPI, LANE, VEC_C>),
                        dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
   return hipGetLastError();
 }
@@ -42,9 +42,16 @@ static hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
 template <bool A_KC, bool B_KC, int VEC>
 static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream) {
   if constexpr (VEC == 1) {
-    // element-load kernels exist up to 128x128 (larger tiles would spill staging registers)
-    if (cfg == kCfg64x64) return launch_f32<A_KC, B_KC, 64, 64, 16, 2, 2, 1, 4>(p, stream);
-    return launch_f32<A_KC, B_KC, 128, 128, 16, 2, 2, 1, 2>(p, stream);
+    // operands or output without 16-byte aligned rows: the DMA tiles with
+    // 4-byte lanes and element stores, or the element-load register-staged
+    // kernels up to 128x128 (larger tiles would spill staging registers)
+    switch (cfg) {
+      case kCfgDma256x256: return launch_dma<A_KC, B_KC, 256, 256, 32, 2, 4, 2, 2, false, 4, false>(p, stream);
+      case kCfgDma256x128: return launch_dma<A_KC, B_KC, 256, 128, 16, 2, 2, 3, 2, false, 4, false>(p, stream);
+      case kCfgDma128x256: return launch_dma<A_KC, B_KC, 128, 256, 16, 2, 2, 3, 2, false, 4, false>(p, stream);
+      case kCfg64x64: return launch_f32<A_KC, B_KC, 64, 64, 16, 2, 2, 1, 4>(p, stream);
+      default: return launch_f32<A_KC, B_KC, 128, 128, 16, 2, 2, 1, 2>(p, stream);
+    }
   } else {
     switch (cfg) {
       case kCfgDma256x256: return launch_dma<A_KC, B_KC, 256, 256, 32, 2, 4, 2, 2>(p, stream);
