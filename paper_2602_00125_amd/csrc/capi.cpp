@@ -160,7 +160,8 @@ int choose_splits(int64_t blocks, int64_t stages, int cfg) {
     return s < 1 ? 1 : (int)s;
   }
   if (blocks >= 512) return 1;
-  int64_t s = cdiv(512, blocks);
+  // two blocks per CU: at most 512 blocks, so that the grid stays one wave
+  int64_t s = 512 / blocks;
   s = std::min<int64_t>(s, stages / 8);
   s = std::min<int64_t>(s, 16);
   return s < 1 ? 1 : (int)s;
