@@ -238,24 +238,32 @@ __global__ __launch_bounds__(kOptThreads) void opt_kernel(const OptBatch b, cons
   const bool vec = b.vec[t] != 0;
   const int tid = threadIdx.x;
   if (vec && c0 + kOptChunk <= n) {
+    // every load of the thread's groups goes out before the first store (the
+    // compiler cannot move a load past a store to a pointer it may alias)
+    constexpr int G = kOptPerThread / 4;
+    f32x4 p4[G], g4[G], a4[G], b4[G];
 #pragma unroll
-    for (int j = 0; j < kOptPerThread / 4; ++j) {
+    for (int j = 0; j < G; ++j) {
       const int64_t i = c0 + ((int64_t)j * kOptThreads + tid) * 4;
-      f32x4 p4 = *(const f32x4*)(th + i);
-      const f32x4 g4 = *(const f32x4*)(g + i);
-      f32x4 a4 = *(const f32x4*)(s1 + i);
-      f32x4 b4 = TWO_STATES ? *(const f32x4*)(s2 + i) : f32x4{};
+      p4[j] = *(const f32x4*)(th + i);
+      g4[j] = *(const f32x4*)(g + i);
+      a4[j] = *(const f32x4*)(s1 + i);
+      b4[j] = TWO_STATES ? *(const f32x4*)(s2 + i) : f32x4{};
+    }
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      const int64_t i = c0 + ((int64_t)j * kOptThreads + tid) * 4;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        float pe = p4[e], ae = a4[e], be = b4[e];
-        op(pe, g4[e], ae, be);
-        p4[e] = pe;
-        a4[e] = ae;
-        b4[e] = be;
+        float pe = p4[j][e], ae = a4[j][e], be = b4[j][e];
+        op(pe, g4[j][e], ae, be);
+        p4[j][e] = pe;
+        a4[j][e] = ae;
+        b4[j][e] = be;
       }
-      *(f32x4*)(th + i) = p4;
-      *(f32x4*)(s1 + i) = a4;
-      if (TWO_STATES) *(f32x4*)(s2 + i) = b4;
+      *(f32x4*)(th + i) = p4[j];
+      *(f32x4*)(s1 + i) = a4[j];
+      if (TWO_STATES) *(f32x4*)(s2 + i) = b4[j];
     }
   } else {
     for (int j = 0; j < kOptPerThread; ++j) {
