@@ -23,7 +23,8 @@ enum GemmCfg {
   kCfgDma256x256w4 = 7,  // the same with 4 waves (128x128 per wave)
   kCfgDma256x128 = 8,    // 256x128, 4 waves, BK = 16 / 32, 3-stage ring (72 KB), 2 blocks per CU
   kCfgDma128x256 = 9,    // 128x256, likewise
-  kNumGemmCfg = 10
+  kCfgDma128x128 = 10,   // 128x128, 4 waves, BK = 32 / 64, 2-stage ring (64 KB), 2 blocks per CU
+  kNumGemmCfg = 11
 };
 int gemm_tile_m(int cfg);
 int gemm_tile_n(int cfg);
