@@ -172,17 +172,19 @@ int choose_splits(int64_t blocks, int64_t stages, int cfg) {
 }
 
 // Tiles that carry the dense-layer-with-nonlinearity epilogue: the 256x256
-// DMA tile for large products, else 128x128 or 64x64 (a forced cfg outside
-// these maps to the nearest of them).
+// DMA tile for large products, else the 128x128 DMA tile (register-staged
+// for unaligned operands) or 64x64 (a forced cfg outside these maps to the
+// nearest of them).
 int choose_epi_cfg(int64_t M, int64_t N, bool vec) {
   auto tiles = [&](int64_t bm, int64_t bn) { return cdiv(M, bm) * cdiv(N, bn); };
   if (g_force_cfg >= 0) {
-    if (g_force_cfg == mt::kCfgDma256x256 && vec) return g_force_cfg;
+    if ((g_force_cfg == mt::kCfgDma256x256 || g_force_cfg == mt::kCfgDma128x128) && vec)
+      return g_force_cfg;
     if (g_force_cfg == mt::kCfg64x64) return g_force_cfg;
     return mt::kCfg128x128;
   }
   if (vec && tiles(256, 256) >= 256) return mt::kCfgDma256x256;
-  if (tiles(128, 128) >= 128) return mt::kCfg128x128;
+  if (tiles(128, 128) >= 128) return vec ? mt::kCfgDma128x128 : mt::kCfg128x128;
   return mt::kCfg64x64;
 }
 

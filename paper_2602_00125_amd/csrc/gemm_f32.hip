@@ -94,9 +94,12 @@ int gemm_tile_k(int cfg, bool bf16) {
 }
 
 // The dense layer followed by a nonlinearity (z / act set): the forward
-// layout only, on the 256x256 DMA tile or the 128x128 / 64x64 tiles.
+// layout only, on the 256x256 or 128x128 DMA tiles or the 128x128 / 64x64
+// register-staged tiles.
 static hipError_t launch_epi(const GemmParams& p, bool vec, int cfg, hipStream_t stream) {
   if (vec) {
+    if (cfg == kCfgDma128x128)
+      return launch_dma<true, true, 128, 128, 32, 2, 2, 2, 2, true>(p, stream);
     if (cfg == kCfgDma256x256)
       return launch_dma<true, true, 256, 256, 32, 2, 4, 2, 2, true>(p, stream);
     if (cfg == kCfg128x128) return launch_f32<true, true, 128, 128, 16, 2, 2, 4, 2, true>(p, stream);

@@ -86,7 +86,7 @@ def test_linear_act_fwd_without_z_and_bf16(kind):
         check_act_out(to_f64(z0), to_f64(y0), Z, S, kind, dtype)
 
 
-@pytest.mark.parametrize("cfg", [6, 3, 4])
+@pytest.mark.parametrize("cfg", [6, 10, 3, 4])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_linear_act_fwd_every_epilogue_tile(cfg, dtype):
     inp = wl.linear(520, 392, 264, dtype=dtype, seed=cfg, dist={"X": ("normal",)}).make()
