@@ -143,9 +143,12 @@ int choose_cfg_aligned(int64_t M, int64_t N, int64_t batch, int64_t stages, bool
   (void)bf16;
   if (tiles(128, 256) >= 512) return N >= M ? mt::kCfg128x256 : mt::kCfg256x128;
   // mid-size products: the 128x128 tile streamed into an LDS ring, two blocks
-  // per CU (measured on 4096 x 1024 x 1024: 103-114 TFLOP/s fp32 against
-  // 88-93 for the register-staged 128x128 tile)
-  const int mid = (vec || !bf16) ? mt::kCfgDma128x128 : mt::kCfg128x128;
+  // per CU (measured on 4096 x 1024 x 1024: 96-106 TFLOP/s fp32 against 88-93
+  // for the register-staged 128x128 tile); fp32 with 16-byte loads takes its
+  // 8-wave form (98-114: one block per CU still has two waves per SIMD), bf16
+  // the 4-wave form (the 8-wave one is 3% slower on dX and dW there)
+  const int mid = vec ? (bf16 ? mt::kCfgDma128x128 : mt::kCfgDma128x128w8)
+                      : (bf16 ? mt::kCfg128x128 : mt::kCfgDma128x128);
   const int64_t t128 = tiles(128, 128);
   if (t128 >= 128) return mid;
   if (can_split && t128 * std::min<int64_t>(16, stages / 8) >= 256) return mid;
@@ -233,6 +236,7 @@ size_t plan_gemm(GemmCall& g, bool may_split) {
   // (4-byte lanes, element stores) and maps the register-staged tiles above
   // 128x128 to them; the element-load register-staged kernels stop at 128x128
   if (!g.vec) {
+    if (g.cfg == mt::kCfgDma128x128w8) g.cfg = mt::kCfgDma128x128;  // 4-byte lanes: 4 waves
     const bool dma = g.cfg == mt::kCfgDma256x256 || g.cfg == mt::kCfgDma256x128 ||
                      g.cfg == mt::kCfgDma128x256 || g.cfg == mt::kCfgDma128x128;
     if (!g.bf16 && (dma || g.cfg == mt::kCfg256x128 || g.cfg == mt::kCfg128x256)) {

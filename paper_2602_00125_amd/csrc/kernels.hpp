@@ -24,7 +24,8 @@ enum GemmCfg {
   kCfgDma256x128 = 8,    // 256x128, 4 waves, BK = 16 / 32, 3-stage ring (72 KB), 2 blocks per CU
   kCfgDma128x256 = 9,    // 128x256, likewise
   kCfgDma128x128 = 10,   // 128x128, 4 waves, BK = 32 / 64, 2-stage ring (64 KB), 2 blocks per CU
-  kNumGemmCfg = 11
+  kCfgDma128x128w8 = 11, // the same tile with 8 waves (32x64 each)
+  kNumGemmCfg = 12
 };
 int gemm_tile_m(int cfg);
 int gemm_tile_n(int cfg);
