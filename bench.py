@@ -34,10 +34,10 @@ METRIC = "TFLOP/s for linear fwd+bwd (3 GEMMs) at M=N=K=8192 fp32; % MFMA peak"
 # sources are stale and not reported)
 KERNEL_SOURCES = {
     "gemm": ["paper_2602_00125_amd/csrc/gemm_kernel.hpp", "paper_2602_00125_amd/csrc/gemm_dma.hpp",
-             "paper_2602_00125_amd/csrc/gemm_f32.hip",
+             "paper_2602_00125_amd/csrc/gemm_dma_body.inc", "paper_2602_00125_amd/csrc/gemm_f32.hip",
              "paper_2602_00125_amd/csrc/gemm_params.hpp", "paper_2602_00125_amd/csrc/capi.cpp"],
     "gemm_bf16": ["paper_2602_00125_amd/csrc/gemm_kernel.hpp", "paper_2602_00125_amd/csrc/gemm_dma.hpp",
-                  "paper_2602_00125_amd/csrc/gemm_bf16.hip",
+                  "paper_2602_00125_amd/csrc/gemm_dma_body.inc", "paper_2602_00125_amd/csrc/gemm_bf16.hip",
                   "paper_2602_00125_amd/csrc/gemm_params.hpp", "paper_2602_00125_amd/csrc/capi.cpp"],
     "colsum": ["paper_2602_00125_amd/csrc/reduce.hip", "paper_2602_00125_amd/csrc/capi.cpp"],
 }
@@ -349,9 +349,11 @@ def cpu_baseline_conv(w, inp, seconds: float):
 
 
 def bench_conv(args, w, inp, dev):
-    """Convolution step: forward (unfold + product with the bias epilogue),
-    then the backward call producing dx, dw and db (dW product on the
-    forward's unfolded input, column sum, dU product, fold)."""
+    """Convolution step: forward (the product gathering the image in its
+    loads, bias epilogue), then the backward call producing dx, dw and db
+    (dW product gathering the image, column sum, dU product, fold). With
+    layouts that cannot gather, the forward unfolds the input into the
+    workspace and the backward's dW reuses it."""
     import torch
 
     from paper_2602_00125_amd import binding as mt
@@ -377,7 +379,7 @@ def bench_conv(args, w, inp, dev):
         mt.conv2d_fwd(x, wt, bias, y, st, pd, workspace=ws)
         if ev is not None:
             ev[1].record()
-        # the backward finds the forward's unfolded input still in the workspace
+        # where the forward unfolded its input, the backward reuses it
         mt.conv2d_bwd(x, wt, dy, dx, dw, db, st, pd, workspace=ws, reuse_unfold=True)
         if ev is not None:
             ev[2].record()

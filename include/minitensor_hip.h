@@ -86,7 +86,11 @@ typedef struct {
                               same x, w, stride and padding (the forward's workspace
                               passed again, untouched since); dw then skips the
                               unfolding. The backward overwrites it (when dx is
-                              asked), so it serves one backward. */
+                              asked), so it serves one backward. Ignored where the
+                              forward may have gathered the image instead (the
+                              layouts listed under mt_conv2d_fwd, C a multiple
+                              of 32): the backward then never reads the unfolded
+                              input, or unfolds it itself. */
 
 /* ------------------------------------------------------------------ linear
  * mt_linear_fwd: Y = X W^T + 1 b^T (Eq. (5); with b == NULL, Eq. (1)).
@@ -220,12 +224,17 @@ mt_status mt_rmsprop_step(int32_t n, const mt_tensor* params, const mt_tensor* g
  *                      [KH][KW][C]; any pitch between output channels
  *   b  [CO] f32 or NULL;  y [N, CO, Ho, Wo] f32 channels-last contiguous
  *                      (memory order N, Ho, Wo, CO)
- * The convolution runs as a product of the unfolded input (a row per output
+ * The convolution runs as a product of the unfolded input U (a row per output
  * pixel, a column per tap) with the flattened weights on the matrix cores.
- * The unfolded input lives in the caller's workspace, which is therefore
- * REQUIRED here (MT_ERR_WORKSPACE without it; size from the *_workspace
- * call: N Ho Wo x round_up(C KH KW, 4) floats, plus split-K partials for dw).
- * fp32 only.
+ * Where x is channels-last (c stride 1, the other strides multiples of 4, a
+ * 16-byte aligned base), w is channels-last and C is a multiple of 32 (the
+ * weight gradient: of 4), with y, w and b allowing 16-byte accesses, the
+ * product's loads gather U's entries from x directly and U is never formed
+ * (the forward's workspace size is then 0). Otherwise U is unfolded into the
+ * caller's workspace, which is REQUIRED for that path (MT_ERR_WORKSPACE
+ * without it; size from the *_workspace call: N Ho Wo x round_up(C KH KW, 4)
+ * floats, plus split-K partials for dw). The backward's dx always goes through
+ * dU = dY Wf in the workspace. fp32 only.
  */
 mt_status mt_conv2d_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* b,
                         const mt_tensor* y, int32_t stride_h, int32_t stride_w, int32_t pad_h,

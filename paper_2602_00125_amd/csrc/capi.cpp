@@ -26,6 +26,7 @@ int g_force_vec1 = 0;
 int g_force_splits = 0;
 int g_force_parts = 0;
 int g_krot = 1;  // K-stage rotation per XCD in the DMA kernel (measured: bf16 NT +2%, others neutral)
+int g_conv_gather = 1;  // convolution products gather the image where the layout allows
 
 mt_status fail(mt_status s, const std::string& msg) {
   g_err = msg;
@@ -206,6 +207,7 @@ struct GemmCall {
   bool vec;   // 16-byte operand loads and output stores
   bool bf16;  // bf16 operands (else fp32)
   int cfg;
+  int conv;   // 1 / 2: A / B gathered from the image (p.cg), else 0
 };
 
 // Whether an operand allows 16-byte loads: `per` elements per vector (4 fp32,
@@ -232,6 +234,8 @@ size_t plan_gemm(GemmCall& g, bool may_split) {
   if (g.cfg < 0)
     g.cfg = choose_cfg(p.M, p.N, p.keep_count, stages_guess, may_split, g.bf16, g.a_kc, g.b_kc,
                        g.vec, p.K, p.red_count);
+  // the gathering convolution kernels exist on the DMA tiles 256x256 and 128x128
+  if (g.conv && !mt::gemm_conv_cfg(g.cfg)) g.cfg = mt::kCfgDma128x128w8;
   // operands or output without 16-byte aligned rows: fp32 keeps the DMA tiles
   // (4-byte lanes, element stores) and maps the register-staged tiles above
   // 128x128 to them; the element-load register-staged kernels stop at 128x128
@@ -283,8 +287,9 @@ mt_status launch_gemm(GemmCall& g, hipStream_t stream, void* ws, size_t ws_bytes
   if (rows_a * p.lda * es >= (int64_t)1 << 31 || rows_b * p.ldb * es >= (int64_t)1 << 31)
     return fail(MT_ERR_LAYOUT, "row pitch too large for 32-bit tile offsets");
   (void)hipGetLastError();  // clear a stale error so the launch check is ours
-  hipError_t e = g.bf16 ? mt::gemm_bf16(p, g.a_kc, g.b_kc, g.vec, g.cfg, stream)
-                        : mt::gemm_f32(p, g.a_kc, g.b_kc, g.vec, g.cfg, stream);
+  hipError_t e = g.conv   ? mt::gemm_f32_conv(p, g.conv, g.cfg, stream)
+                 : g.bf16 ? mt::gemm_bf16(p, g.a_kc, g.b_kc, g.vec, g.cfg, stream)
+                          : mt::gemm_f32(p, g.a_kc, g.b_kc, g.vec, g.cfg, stream);
   if (e != hipSuccess) return hip_status(e);
   if (p.splits > 1) {
     // batch elements of C are contiguous M x N blocks when batched (mt_matmul)
@@ -845,6 +850,45 @@ mt_status conv_plan(const mt_tensor* x, const mt_tensor* w, int32_t sh, int32_t 
   return MT_OK;
 }
 
+// (mag, shift) with n / d = (n * mag) >> shift for every n < 2^31: shift =
+// 31 + ceil(log2 d), mag = ceil(2^shift / d), which stays below 2^32.
+void fast_div_params(int64_t d, uint32_t* mag, int32_t* shift) {
+  int l = 0;
+  while (((int64_t)1 << l) < d) ++l;
+  const int s = 31 + l;
+  *mag = (uint32_t)((((uint64_t)1 << s) + (uint64_t)d - 1) / (uint64_t)d);
+  *shift = s;
+}
+
+// Whether a convolution product may gather the image in its loads instead of
+// reading the unfolded matrix (mode 1: the forward, whose K-stages are whole
+// groups of 32 channels of one tap; mode 2: the weight gradient, 4-channel
+// chunks), and the description the kernels take. Needs channels-last x and
+// weights (k = (u, v, c)), 16-byte aligned pixels, 32-bit offsets into x.
+bool conv_gather(const ConvPlan& cp, const mt_tensor* x, int mode, mt::ConvGather* cg) {
+  const mt::ConvGeom& g = cp.g;
+  if (!g_conv_gather || g_force_vec1 || !g.korder_uvc || g.xs[1] != 1) return false;
+  if (g.C % (mode == 1 ? 32 : 4) != 0) return false;
+  if (!aligned16(x->data) || g.xs[0] % 4 || g.xs[2] % 4 || g.xs[3] % 4) return false;
+  const int64_t lim = (int64_t)1 << 14;
+  if (g.H >= lim || g.W >= lim || g.KH >= lim || g.KW >= lim || g.ph >= lim || g.pw >= lim)
+    return false;
+  const int64_t ext = (int64_t)(g.N - 1) * g.xs[0] + (int64_t)(g.H - 1) * g.xs[2] +
+                      (int64_t)(g.W - 1) * g.xs[3] + g.C;
+  if (ext + (int64_t)g.ph * g.xs[2] + (int64_t)g.pw * g.xs[3] >= ((int64_t)1 << 29)) return false;
+  if (cp.M >= ((int64_t)1 << 31) - 64) return false;
+  std::memset(cg, 0, sizeof(*cg));
+  cg->x = (const float*)x->data;
+  cg->x_bytes = (uint32_t)(ext * 4);
+  cg->C = g.C; cg->H = g.H; cg->W = g.W; cg->KW = g.KW;
+  cg->sh = g.sh; cg->sw = g.sw; cg->ph = g.ph; cg->pw = g.pw;
+  cg->HO = g.HO; cg->WO = g.WO;
+  cg->xs0 = (int32_t)g.xs[0]; cg->xs2 = (int32_t)g.xs[2]; cg->xs3 = (int32_t)g.xs[3];
+  fast_div_params(g.WO, &cg->wo_mag, &cg->wo_shift);
+  fast_div_params(g.HO, &cg->ho_mag, &cg->ho_shift);
+  return true;
+}
+
 mt_status check_act4(const mt_tensor* t, const char* name, int64_t N, int64_t C, int64_t H,
                      int64_t W) {
   mt_status s = check_tensor(t, name, 4, 4);
@@ -867,20 +911,8 @@ mt_status conv_fwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
   if (b && (s = check_vector(b, "b", g.CO))) return s;
   if (overlaps(y, x) || overlaps(y, w) || overlaps(y, b))
     return fail(MT_ERR_ALIAS, "y overlaps an input");
-  if (ws_query) {
-    *ws_query = cp.col_bytes;
-    return MT_OK;
-  }
-  if (cp.M == 0) return MT_OK;
-  if (!ws || ws_bytes < cp.col_bytes || ((uintptr_t)ws & 255))
-    return fail(MT_ERR_WORKSPACE, "convolution: needs a 256-byte aligned workspace of "
-                                  "mt_conv2d_fwd_workspace bytes (the unfolded input)");
-  float* col = (float*)ws;
-  (void)hipGetLastError();
-  if ((s = hip_status(mt::conv_unfold((const float*)x->data, g, col, stream)))) return s;
   GemmCall gc{};
   init_params(&gc.p);
-  gc.p.a = col;
   gc.p.b = w->data;
   gc.p.c = (float*)y->data;
   gc.p.bias = b ? (const float*)b->data : nullptr;
@@ -896,6 +928,27 @@ mt_status conv_fwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
   gc.vec = g.Kc % 4 == 0 && vec_ok_operand(w->data, g.CO, g.Kc, cp.wpitch, nullptr, 0, 4) &&
            aligned16(y->data) && g.CO % 4 == 0 && (!gc.p.bias || aligned16(gc.p.bias));
   gc.cfg = -1;
+  // the product reads the image itself where it can, else the unfolded input
+  // in the workspace
+  const bool gather = gc.vec && conv_gather(cp, x, 1, &gc.p.cg);
+  if (ws_query) {
+    *ws_query = gather ? 0 : cp.col_bytes;
+    return MT_OK;
+  }
+  if (cp.M == 0) return MT_OK;
+  if (gather) {
+    gc.conv = 1;
+    gc.p.a = x->data;
+    gc.p.lda = 0;
+    return launch_gemm(gc, stream, nullptr, 0);
+  }
+  if (!ws || ws_bytes < cp.col_bytes || ((uintptr_t)ws & 255))
+    return fail(MT_ERR_WORKSPACE, "convolution: needs a 256-byte aligned workspace of "
+                                  "mt_conv2d_fwd_workspace bytes (the unfolded input)");
+  float* col = (float*)ws;
+  (void)hipGetLastError();
+  if ((s = hip_status(mt::conv_unfold((const float*)x->data, g, col, stream)))) return s;
+  gc.p.a = col;
   return launch_gemm(gc, stream, nullptr, 0);
 }
 
@@ -965,6 +1018,11 @@ mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
     gdw.vec = g.CO % 4 == 0 && g.Kc % 4 == 0 && aligned16(dy->data) && aligned16(dw->data) &&
               dwpitch % 4 == 0;
     gdw.cfg = -1;
+    if (gdw.vec && conv_gather(cp, x, 2, &gdw.p.cg)) {
+      gdw.conv = 2;
+      gdw.p.b = x->data;
+      gdw.p.ldb = 0;
+    }
     GemmCall probe = gdw;
     need_dw = plan_gemm(probe, true);
   }
@@ -974,25 +1032,33 @@ mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
     parts = g_force_parts > 0 ? g_force_parts : mt::colsum_parts(cp.M, g.CO);
     if (parts > 1) need_db = (size_t)parts * g.CO * sizeof(float);
   }
-  const size_t need = ((dw || dx) ? cp.col_bytes : 0) + std::max(need_dw, need_db);
+  // the unfolded matrix (U for an unfolded dW, then dU for dx) heads the
+  // workspace, the split partials follow
+  const size_t col_need = (dx || (dw && !gdw.conv)) ? cp.col_bytes : 0;
+  const size_t need = col_need + std::max(need_dw, need_db);
   if (ws_query) {
     *ws_query = need;
     return MT_OK;
   }
-  if ((dw || dx) && cp.M > 0 && (!ws || ws_bytes < cp.col_bytes || ((uintptr_t)ws & 255)))
+  if (col_need && cp.M > 0 && (!ws || ws_bytes < col_need || ((uintptr_t)ws & 255)))
     return fail(MT_ERR_WORKSPACE, "convolution: needs a 256-byte aligned workspace of "
                                   "mt_conv2d_bwd_workspace bytes (the unfolded input)");
   if (ws && ((uintptr_t)ws & 255)) return fail(MT_ERR_WORKSPACE, "workspace must be 256-byte aligned");
   float* col = (float*)ws;
-  char* rest = ws ? (char*)ws + cp.col_bytes : nullptr;
-  const size_t rest_bytes = ws && ws_bytes > cp.col_bytes ? ws_bytes - cp.col_bytes : 0;
+  char* rest = ws ? (char*)ws + col_need : nullptr;
+  const size_t rest_bytes = ws && ws_bytes > col_need ? ws_bytes - col_need : 0;
   (void)hipGetLastError();
-  if (dw) {
-    // MT_CONV_REUSE_UNFOLD: the forward left the unfolded input at the start of ws
-    if (cp.M > 0 && !(flags & MT_CONV_REUSE_UNFOLD) &&
+  if (dw && !gdw.conv) {
+    // MT_CONV_REUSE_UNFOLD: the forward left the unfolded input at the start
+    // of ws, unless that forward gathered the image (then nothing is there)
+    mt::ConvGather unused;
+    const bool reuse = (flags & MT_CONV_REUSE_UNFOLD) && !conv_gather(cp, x, 1, &unused);
+    if (cp.M > 0 && !reuse &&
         (s = hip_status(mt::conv_unfold((const float*)x->data, g, col, stream))))
       return s;
     gdw.p.b = col;
+    if ((s = launch_gemm(gdw, stream, rest_bytes ? rest : nullptr, rest_bytes))) return s;
+  } else if (dw) {
     if ((s = launch_gemm(gdw, stream, rest_bytes ? rest : nullptr, rest_bytes))) return s;
   }
   if (db) {
@@ -1320,6 +1386,9 @@ int mt_debug_set(const char* key, int64_t value) {
   } else if (!std::strcmp(key, "krot")) {
     if (value < 0 || value > 1) return -2;
     g_krot = (int)value;
+  } else if (!std::strcmp(key, "conv_gather")) {
+    if (value < 0 || value > 1) return -2;
+    g_conv_gather = (int)value;
   } else if (!std::strcmp(key, "splits") || !std::strcmp(key, "parts")) {
     if (value < 0 || value > 4096) return -2;
     (key[0] == 's' ? g_force_splits : g_force_parts) = (int)value;

@@ -41,6 +41,8 @@
 #pragma once
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "gemm_kernel.hpp"
 #include "gemm_params.hpp"
 
@@ -201,6 +203,146 @@ struct DmaLoader {
   }
 };
 
+// q = n / d for n < 2^31 from the host's (mag, shift) of d.
+__device__ __forceinline__ uint32_t fast_div(uint32_t n, uint32_t mag, int shift) {
+  return (uint32_t)(((uint64_t)n * mag) >> shift);
+}
+
+// Convolution, forward product: A is the unfolded input U (rows m = output
+// pixels, K-contiguous), gathered from the image. A stage covers BK channels
+// of one tap (u, v) (C is a multiple of BK), so a lane's 16-byte chunk is 4
+// consecutive channels of one input pixel: contiguous in channels-last x.
+// Per lane and load the pixel's window origin is decoded once per block; per
+// stage the tap moves, and a chunk whose input pixel falls in the padding (or
+// whose row lies past the last pixel) reads zero.
+template <int BM, int BK, int NW>
+struct ConvGatherA {
+  using T = DmaTile<4, true, BM, BK>;
+  static constexpr int IB = 1024;
+  static constexpr int JB = T::BYTES / IB / NW;
+  static_assert(T::BYTES % (IB * NW) == 0, "instructions split evenly over the waves");
+  static constexpr int32_t kFar = -(1 << 30);  // window origin of rows past the last pixel
+  int32_t base[JB];  // element offset of the chunk at tap (0, 0), channel group 0
+  int32_t hb[JB], wb[JB];  // input row / column of the window's tap (0, 0)
+
+  __device__ __forceinline__ void init(int wave, int lane, const ConvGather& g, int64_t m0,
+                                       int64_t M) {
+#pragma unroll
+    for (int j = 0; j < JB; ++j) {
+      const int byte = IB * (wave + NW * j) + 16 * lane;
+      const int r = byte / T::RB;
+      const int c = (((byte % T::RB) / 16) ^ T::swz(r)) * 4;
+      const int64_t m = m0 + r;
+      if (m < M) {
+        const uint32_t t = fast_div((uint32_t)m, g.wo_mag, g.wo_shift);
+        const int32_t jj = (int32_t)((uint32_t)m - t * (uint32_t)g.WO);
+        const uint32_t n = fast_div(t, g.ho_mag, g.ho_shift);
+        const int32_t i = (int32_t)(t - n * (uint32_t)g.HO);
+        hb[j] = i * g.sh - g.ph;
+        wb[j] = jj * g.sw - g.pw;
+        base[j] = (int32_t)n * g.xs0 + hb[j] * g.xs2 + wb[j] * g.xs3 + c;
+      } else {
+        hb[j] = kFar;
+        wb[j] = 0;
+        base[j] = 0;
+      }
+    }
+  }
+  struct Plan {
+    __amdgpu_buffer_rsrc_t r;
+    int32_t toff;  // element offset of tap (u, v), channel c0
+    int32_t u, v;
+    uint32_t lds0;
+  };
+  __device__ __forceinline__ Plan plan(const ConvGather& g, bool live, int u, int v, int c0,
+                                       char* lds) const {
+    Plan q;
+    q.r = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(g.x), (short)0,
+                                            live ? (int)g.x_bytes : 0, kRsrcWord3);
+    q.toff = u * g.xs2 + v * g.xs3 + c0;
+    q.u = u;
+    q.v = v;
+    q.lds0 = lds_byte_addr(lds);
+    return q;
+  }
+  __device__ __forceinline__ void issue_one(const Plan& q, int j, int wave,
+                                            const ConvGather& g) const {
+    const int32_t h = hb[j] + q.u, w = wb[j] + q.v;
+    const bool ok = (uint32_t)h < (uint32_t)g.H && (uint32_t)w < (uint32_t)g.W;
+    const uint32_t o = ok ? (uint32_t)(base[j] + q.toff) * 4u : kOOB;
+    dma16(q.r, o, q.lds0 + IB * (wave + NW * j));
+  }
+};
+
+// Convolution, weight gradient: B is U again, now with the pixels m as the
+// contraction (tile rows, BK per stage) and the unfolded columns k as tile
+// columns. A lane's chunk keeps its column, so its tap (u, v) and channel are
+// decoded once per block (C % 4 == 0 keeps a chunk inside one tap); per
+// stage its row's pixel is decoded (two divisions by multiplication).
+template <int BN, int BK, int NW>
+struct ConvGatherB {
+  using T = DmaTile<4, false, BN, BK>;
+  static constexpr int IB = 1024;
+  static constexpr int JB = T::BYTES / IB / NW;
+  static_assert(T::BYTES % (IB * NW) == 0, "instructions split evenly over the waves");
+  // tap row of columns past the last: beyond any input row (H + ph < 2^14)
+  static constexpr int32_t kFarTap = 0x7fff;
+  uint32_t ch[JB];  // channel of the chunk's first column
+  uint32_t uv[JB];  // tap u | v << 16
+  uint32_t rr[JB];  // row (pixel) within the stage
+
+  __device__ __forceinline__ void init(int wave, int lane, const ConvGather& g, int64_t n0,
+                                       int64_t N) {
+#pragma unroll
+    for (int j = 0; j < JB; ++j) {
+      const int byte = IB * (wave + NW * j) + 16 * lane;
+      const int r = byte / T::RB;
+      const int c = (((byte % T::RB) / 16) ^ T::swz(r)) * 4;
+      const int64_t col = n0 + c;
+      rr[j] = (uint32_t)r;
+      if (col < N) {
+        const uint32_t tap = (uint32_t)col / (uint32_t)g.C;
+        const uint32_t u = tap / (uint32_t)g.KW;
+        ch[j] = (uint32_t)col - tap * (uint32_t)g.C;
+        uv[j] = u | ((tap - u * (uint32_t)g.KW) << 16);
+      } else {
+        ch[j] = 0;
+        uv[j] = (uint32_t)kFarTap;
+      }
+    }
+  }
+  struct Plan {
+    __amdgpu_buffer_rsrc_t r;
+    uint32_t m0;    // first pixel of the stage
+    uint32_t mlim;  // number of pixels (the contraction length)
+    uint32_t lds0;
+  };
+  __device__ __forceinline__ Plan plan(const ConvGather& g, bool live, uint32_t m0, uint32_t mlim,
+                                       char* lds) const {
+    Plan q;
+    q.r = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(g.x), (short)0,
+                                            live ? (int)g.x_bytes : 0, kRsrcWord3);
+    q.m0 = m0;
+    q.mlim = mlim;
+    q.lds0 = lds_byte_addr(lds);
+    return q;
+  }
+  __device__ __forceinline__ void issue_one(const Plan& q, int j, int wave,
+                                            const ConvGather& g) const {
+    const uint32_t m = q.m0 + rr[j];
+    const uint32_t t = fast_div(m, g.wo_mag, g.wo_shift);
+    const uint32_t jj = m - t * (uint32_t)g.WO;
+    const uint32_t n = fast_div(t, g.ho_mag, g.ho_shift);
+    const uint32_t i = t - n * (uint32_t)g.HO;
+    const uint32_t h = i * (uint32_t)g.sh - (uint32_t)g.ph + (uv[j] & 0xffffu);
+    const uint32_t w = jj * (uint32_t)g.sw - (uint32_t)g.pw + (uv[j] >> 16);
+    const bool ok = m < q.mlim && h < (uint32_t)g.H && w < (uint32_t)g.W;
+    const uint32_t o =
+        ok ? (n * (uint32_t)g.xs0 + h * (uint32_t)g.xs2 + w * (uint32_t)g.xs3 + ch[j]) * 4u : kOOB;
+    dma16(q.r, o, q.lds0 + IB * (wave + NW * j));
+  }
+};
+
 // Fragment loads and MFMAs of one k-step, split so that the next k-step's
 // fragments load while the current k-step multiplies, and the MFMAs in
 // chunks between which the kernel places its loads.
@@ -309,294 +451,20 @@ template <typename T, bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int
 __global__ __launch_bounds__(WGM * WGN * 64)
 __attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
 void gemm_dma_kernel(const GemmParams p) {
-  constexpr int ES = (int)sizeof(T);
-  constexpr int NW = WGM * WGN;
-  constexpr int WTM = BM / WGM, WTN = BN / WGN;
-  constexpr int TM = WTM / 32, TN = WTN / 32;
-  static_assert(NS >= 2 && NS <= 5, "a ring of two to five stages");
-  using LA = DmaLoader<ES, A_KC, BM, BK, NW, DMA_LANE>;
-  using LB = DmaLoader<ES, B_KC, BN, BK, NW, DMA_LANE>;
-  constexpr int A_BYTES = LA::T::BYTES, B_BYTES = LB::T::BYTES;
-  constexpr int STAGE = A_BYTES + B_BYTES;
-  constexpr int L = LA::JB + LB::JB;  // DMA instructions per wave per stage
-  __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
+  constexpr int CONV = 0;
+#include "gemm_dma_body.inc"
+}
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (LDS DMA base)
-  const int wm = wave / WGN, wn = wave % WGN;
-  const int l32 = lane & 31, h = lane >> 5;
-
-  // ---- block -> (split, batch, tile), as in gemm_kernel
-  const int64_t tiles = (int64_t)p.tiles_m * p.tiles_n;
-  int64_t logical = xcd_remap(blockIdx.x, gridDim.x);
-  const int64_t t = logical % tiles;
-  logical /= tiles;
-  const int64_t batch = logical % p.keep_count;
-  const int split = (int)(logical / p.keep_count);
-  int tm_idx, tn_idx;
-  {
-    const int64_t width = (int64_t)p.group_m * p.tiles_n;
-    const int64_t gid = t / width;
-    const int64_t first = gid * p.group_m;
-    const int64_t gsz = (p.tiles_m - first) < p.group_m ? (p.tiles_m - first) : p.group_m;
-    tm_idx = (int)(first + (t % width) % gsz);
-    tn_idx = (int)((t % width) / gsz);
-  }
-  const int64_t m0 = (int64_t)tm_idx * BM, n0 = (int64_t)tn_idx * BN;
-  int64_t a_off = 0, b_off = 0, c_off = 0;
-  {
-    int64_t rem = batch;
-    for (int d = p.nkeep - 1; d >= 0; --d) {
-      const int64_t i = rem % p.keep_shape[d];
-      rem /= p.keep_shape[d];
-      a_off += i * p.keep_sa[d];
-      b_off += i * p.keep_sb[d];
-      c_off += i * p.keep_sc[d];
-    }
-  }
-  const char* A = (const char*)p.a + a_off * ES;
-  const char* B = (const char*)p.b + b_off * ES;
-
-  const int64_t KS = (p.K + BK - 1) / BK;
-  const int64_t S_all = KS * p.red_count;
-  const int64_t st0 = (int64_t)split * p.stages_per_split;
-  const int64_t st1 = (st0 + p.stages_per_split) < S_all ? (st0 + p.stages_per_split) : S_all;
-  const int S = st1 > st0 ? (int)(st1 - st0) : 0;
-
-  LA la;
-  LB lb;
-  la.init(wave, lane, p.lda, p.M - m0);
-  lb.init(wave, lane, p.ldb, p.N - n0);
-
-  // issue cursor: (summed batch index r, k tile kt) of the next stage to
-  // load, wave-uniform (scalar registers)
-  int64_t cur_r = uniform_i64(KS > 0 ? st0 / KS : 0);
-  int64_t cur_kt = uniform_i64(KS > 0 ? st0 % KS : 0);
-  int64_t ra_off = 0, rb_off = 0;
-  auto red_offsets = [&](int64_t r) {
-    ra_off = 0;
-    rb_off = 0;
-    for (int d = p.nred - 1; d >= 0; --d) {
-      const int64_t i = r % p.red_shape[d];
-      r /= p.red_shape[d];
-      ra_off += i * p.red_sa[d];
-      rb_off += i * p.red_sb[d];
-    }
-  };
-  if (S > 0 && p.nred > 0) red_offsets(cur_r);
-  // tile origins of the next stage to load, advanced by one K-stage per
-  // load; recomputed only where the summed batch index moves on
-  const int64_t a_step = (A_KC ? (int64_t)BK : (int64_t)BK * p.lda) * ES;
-  const int64_t b_step = (B_KC ? (int64_t)BK : (int64_t)BK * p.ldb) * ES;
-  const char* a_nxt = A;
-  const char* b_nxt = B;
-  int64_t k_left = 0;
-  auto seek = [&]() {
-    const int64_t k0 = cur_kt * BK;
-    a_nxt = uniform_ptr(A + (ra_off + (A_KC ? m0 * p.lda + k0 : k0 * p.lda + m0)) * ES);
-    b_nxt = uniform_ptr(B + (rb_off + (B_KC ? n0 * p.ldb + k0 : k0 * p.ldb + n0)) * ES);
-    k_left = uniform_i64(p.K - k0);
-  };
-  // K-stage rotation (p.krot): the sequence starts at stage rot and wraps to
-  // stage 0 once, where the tile origins are sought again
-  bool wrap_pending = false;
-  if (p.krot && p.splits == 1 && p.red_count == 1 && KS > 1) {
-    const int64_t rot = ((int64_t)(blockIdx.x & 7) * KS) >> 3;
-    if (rot > 0) {
-      cur_kt = uniform_i64(rot);
-      wrap_pending = true;
-    }
-  }
-  if (S > 0) seek();
-  // plans of the next stage's loads (into LDS slot `slot`); advances the cursor
-  typename LA::Plan pa;
-  typename LB::Plan pb;
-  // Stages past the last (planned while the final NS-1 stages compute) load
-  // nothing: every chunk is out of range and reads zero into a slot no wave
-  // reads again, so the loop issues the same loads in every stage, unbranched.
-  int planned = 0;
-  auto plan_next = [&](int slot) {
-    char* dst = lds + slot * STAGE;
-    const bool live = planned < S;
-    ++planned;
-    pa = la.plan(a_nxt, k_left, dst, live);
-    pb = lb.plan(b_nxt, k_left, dst + A_BYTES, live);
-    if (++cur_kt == KS) {
-      cur_kt = 0;
-      if (wrap_pending) {
-        wrap_pending = false;
-        seek();
-      } else {
-        ++cur_r;
-        if (cur_r < p.red_count) {
-          red_offsets(cur_r);
-          seek();
-        }
-      }
-    } else {
-      a_nxt += a_step;
-      b_nxt += b_step;
-      k_left -= BK;
-    }
-  };
-  // the j-th (of L) load of the planned stage: A's first, then B's
-  auto issue_one = [&](int j) {
-    if (j < LA::JB) la.template issue_one<KTAIL>(pa, j, wave);
-    else lb.template issue_one<KTAIL>(pb, j - LA::JB, wave);
-  };
-
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
-
-  using Mma = DmaMma<T, A_KC, B_KC, TM, TN, BK, BM, BN>;
-  typename Mma::Frags cur, nxt;
-  const int am = wm * WTM, bn = wn * WTN;
-
-  // prologue: stages 0 .. NS-2 in flight
-#pragma unroll
-  for (int q = 0; q < NS - 1; ++q) {
-    plan_next(q);
-#pragma unroll
-    for (int j = 0; j < L; ++j) issue_one(j);
-  }
-
-  constexpr int CHUNKS = Mma::CHUNKS;
-  static_assert(DMA_G0 >= 0 && DMA_GS >= 1 && DMA_G0 < Mma::KSTEPS * CHUNKS, "issue points");
-  // issue points: chunks DMA_G0, DMA_G0 + DMA_GS, ... of the stage; PER loads at each
-  constexpr int POINTS = (Mma::KSTEPS * CHUNKS - DMA_G0 + DMA_GS - 1) / DMA_GS;
-  constexpr int PER = (L + POINTS - 1) / POINTS;
-  // one stage; the loads of stage s+NS-1 go out during it
-  auto run_stage = [&](int s) {
-    // stages 0 .. s+NS-2 have been issued: this wave's loads of stage s have
-    // landed once at most NS-2 later stages (of L loads each) are in flight;
-    // the barrier then makes every wave's loads visible and frees the slot
-    // stage s-1 used
-    wait_vmcnt<(NS - 2) * L>();
-    __builtin_amdgcn_s_barrier();
-    __asm__ __volatile__("" ::: "memory");
-    const char* st = lds + (s % NS) * STAGE;
-    Mma::load(st, st + A_BYTES, am, bn, lane, 0, cur);
-#pragma unroll
-    for (int ks = 0; ks < Mma::KSTEPS; ++ks) {
-      if (ks + 1 < Mma::KSTEPS) Mma::load(st, st + A_BYTES, am, bn, lane, ks + 1, nxt);
-#pragma unroll
-      for (int c = 0; c < CHUNKS; ++c) {
-        Mma::compute_chunk(cur, acc, c);
-        // the next stage's L loads go out PER at a time after every
-        // DMA_GS-th chunk of MFMAs from chunk DMA_G0 on, so that no wave
-        // stalls on a burst of loads the memory pipeline cannot take at once
-        const int g = ks * CHUNKS + c;
-        if (g >= DMA_G0 && (g - DMA_G0) % DMA_GS == 0 && (g - DMA_G0) / DMA_GS * PER < L) {
-          if (g == DMA_G0) plan_next((s + NS - 1) % NS);
-          const int j0 = (g - DMA_G0) / DMA_GS * PER;
-#pragma unroll
-          for (int j = j0; j < j0 + PER && j < L; ++j) issue_one(j);
-        }
-        // keep each chunk's MFMAs and loads where they are: left to itself
-        // the scheduler gathers the loads into bursts again
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      cur = nxt;
-    }
-    __asm__ __volatile__("" ::: "memory");
-  };
-  for (int s = 0; s < S; ++s) run_stage(s);
-  // the empty loads of the stages past the last land before the wave ends
-  wait_vmcnt<0>();
-
-  // ---- epilogue (as in gemm_kernel): lane holds C[m][n0' + 8g + 4h + 0..3]
-  if constexpr (EPI) {
-    act_epilogue<TM, TN, true>(p, acc, m0 + wm * WTM + l32, n0 + wn * WTN + 4 * h);
-    return;
-  }
-  const bool to_partial = p.splits > 1;
-  float* C = to_partial ? p.partial + (int64_t)split * p.partial_stride + batch * p.M * p.N
-                        : p.c + c_off;
-  const int64_t ldc = to_partial ? p.N : p.ldc;
-  if constexpr (!VEC_C) {
-    // Rows of C not 16-byte aligned (odd pitch or N): each wave stages 32
-    // rows of its tile at a time in its own slice of the (now idle) ring,
-    // then writes them back a row at a time, 64 lanes on 64 consecutive
-    // columns: one contiguous 256-byte store per row segment instead of
-    // scattered 4-byte stores. Row pitch WTN + 4 floats offsets consecutive
-    // rows by 16 bytes in the LDS banks.
-    constexpr int SP = WTN + 4;
-    static_assert(NW * 32 * SP * 4 <= NS * STAGE, "staging fits in the ring");
-    __syncthreads();  // every wave has finished reading the ring
-    float* stg = (float*)(lds + wave * 32 * SP * 4);
-    const int64_t mb = m0 + wm * WTM, nb = n0 + wn * WTN;
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-#pragma unroll
-      for (int q = 0; q < TN; ++q)
-#pragma unroll
-        for (int g = 0; g < 4; ++g)
-          *(f32x4*)&stg[l32 * SP + q * 32 + 8 * g + 4 * h] =
-              f32x4{acc[i][q][4 * g + 0], acc[i][q][4 * g + 1], acc[i][q][4 * g + 2],
-                    acc[i][q][4 * g + 3]};
-      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes done
-      __builtin_amdgcn_wave_barrier();
-#pragma unroll 4
-      for (int r = 0; r < 32; ++r) {
-        const int64_t m = mb + i * 32 + r;
-        if (m >= p.M) break;
-        float* crow = C + m * ldc;
-#pragma unroll
-        for (int cb = 0; cb < WTN; cb += 64) {
-          const int64_t n = nb + cb + lane;
-          if (n >= p.N) continue;
-          float x = stg[r * SP + cb + lane];
-          if (!to_partial) {
-            if (p.bias) x += p.bias[n];
-            if (p.accumulate) x += crow[n];
-          }
-          crow[n] = x;
-        }
-      }
-      __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the next slab overwrites
-      __builtin_amdgcn_wave_barrier();
-    }
-    return;
-  }
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int64_t m = m0 + wm * WTM + i * 32 + l32;
-    if (m >= p.M) continue;
-    float* crow = C + m * ldc;
-#pragma unroll
-    for (int q = 0; q < TN; ++q) {
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int64_t n = n0 + wn * WTN + q * 32 + 8 * g + 4 * h;
-        if constexpr (!VEC_C) {
-          // rows of C not 16-byte aligned (odd pitch or N): element stores
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            if (n + e >= p.N) continue;
-            float x = acc[i][q][4 * g + e];
-            if (!to_partial) {
-              if (p.bias) x += p.bias[n + e];
-              if (p.accumulate) x += crow[n + e];
-            }
-            crow[n + e] = x;
-          }
-          continue;
-        }
-        if (n >= p.N) continue;
-        f32x4 v = {acc[i][q][4 * g + 0], acc[i][q][4 * g + 1], acc[i][q][4 * g + 2],
-                   acc[i][q][4 * g + 3]};
-        if (!to_partial) {
-          if (p.bias) v += *(const f32x4*)&p.bias[n];
-          if (p.accumulate) v += *(const f32x4*)&crow[n];
-        }
-        *(f32x4*)&crow[n] = v;
-      }
-    }
-  }
+// The convolution products with the image gathered by the loads: CONV_ 1 the
+// forward (y = U Wf^T + b, NT), 2 the weight gradient (dW = dY^T U, TN).
+template <int CONV_, int BM, int BN, int BK, int WGM, int WGN, int NS, bool KTAIL, int WAVES_PER_EU>
+__global__ __launch_bounds__(WGM * WGN * 64)
+__attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
+void conv_dma_kernel(const GemmParams p) {
+  using T = float;
+  constexpr bool A_KC = CONV_ == 1, B_KC = CONV_ == 1, EPI = false, VEC_C = true;
+  constexpr int DMA_G0 = 1, DMA_GS = 1, DMA_LANE = 16, CONV = CONV_;
+#include "gemm_dma_body.inc"
 }
 
 }  // namespace gemm

@@ -113,6 +113,47 @@ static hipError_t launch_epi(const GemmParams& p, bool vec, int cfg, hipStream_t
   return launch_f32<true, true, 64, 64, 16, 2, 2, 1, 4, true>(p, stream);
 }
 
+template <int MODE, int BM, int BN, int BK, int WGM, int WGN, int NS, int WPE>
+static hipError_t launch_conv(const GemmParams& p, hipStream_t stream) {
+  GemmParams q = p;
+  q.tiles_m = (int32_t)((p.M + BM - 1) / BM);
+  q.tiles_n = (int32_t)((p.N + BN - 1) / BN);
+  const int64_t blocks = (int64_t)q.tiles_m * q.tiles_n * p.keep_count * p.splits;
+  if (blocks <= 0) return hipSuccess;
+  if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
+  if (p.K % BK != 0) {
+    // the forward's stages are whole channel groups of one tap
+    if constexpr (MODE == 1) return hipErrorInvalidValue;
+    else
+      hipLaunchKernelGGL((gemm::conv_dma_kernel<MODE, BM, BN, BK, WGM, WGN, NS, true, WPE>),
+                         dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
+  } else {
+    hipLaunchKernelGGL((gemm::conv_dma_kernel<MODE, BM, BN, BK, WGM, WGN, NS, false, WPE>),
+                       dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
+  }
+  return hipGetLastError();
+}
+
+template <int MODE>
+static hipError_t conv_cfg(const GemmParams& p, int cfg, hipStream_t stream) {
+  switch (cfg) {
+    case kCfgDma256x256: return launch_conv<MODE, 256, 256, 32, 2, 4, 2, 2>(p, stream);
+    case kCfgDma128x128: return launch_conv<MODE, 128, 128, 32, 2, 2, 2, 2>(p, stream);
+    case kCfgDma128x128w8: return launch_conv<MODE, 128, 128, 32, 4, 2, 2, 4>(p, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+bool gemm_conv_cfg(int cfg) {
+  return cfg == kCfgDma256x256 || cfg == kCfgDma128x128 || cfg == kCfgDma128x128w8;
+}
+
+hipError_t gemm_f32_conv(const GemmParams& p, int mode, int cfg, hipStream_t stream) {
+  if (mode == 1) return conv_cfg<1>(p, cfg, stream);
+  if (mode == 2) return conv_cfg<2>(p, cfg, stream);
+  return hipErrorInvalidValue;
+}
+
 hipError_t gemm_f32(const GemmParams& p, bool a_kc, bool b_kc, bool vec, int cfg,
                     hipStream_t stream) {
   if (p.act || p.z) {

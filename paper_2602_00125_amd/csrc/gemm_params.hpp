@@ -15,6 +15,23 @@ namespace mt {
 
 constexpr int kMaxBatchDims = 6;
 
+// A convolution operand that the GEMM loads gather from the image instead of
+// reading an unfolded matrix (MiniTensor Sec. 3.3 Eq. (6)): x is stored
+// channels-last (c has stride 1), the unfolded columns run k = (u, v, c) with
+// c fastest, and output pixel m = (n, i, j) reads input pixel
+// (n, i sh - ph + u, j sw - pw + v), zero outside the image. Divisions by WO
+// and HO use q = (m * mag) >> shift, exact for m < 2^31.
+struct ConvGather {
+  const float* x;
+  uint32_t x_bytes;  // bytes from x that the loads may read (buffer bound)
+  int32_t C, H, W, KW;
+  int32_t sh, sw, ph, pw;
+  int32_t HO, WO;
+  int32_t xs0, xs2, xs3;  // element strides of x over n, h, w
+  uint32_t wo_mag, ho_mag;
+  int32_t wo_shift, ho_shift;
+};
+
 struct GemmParams {
   const void* a;
   const void* b;
@@ -54,6 +71,9 @@ struct GemmParams {
   // XCD x start their K loop at stage x * KS / 8 and wrap around, so that the
   // eight XCDs stream different columns of the operands at any one time
   int32_t krot;
+  // convolution kernels only: the gathered operand (A of the forward product,
+  // B of the weight gradient); every other kernel ignores it
+  ConvGather cg;
 };
 
 }  // namespace mt

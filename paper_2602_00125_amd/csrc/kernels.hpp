@@ -35,6 +35,12 @@ int gemm_tile_k(int cfg, bool bf16);
 // contiguous extent, pitch, batch stride and base allows them); else 4-byte.
 hipError_t gemm_f32(const GemmParams& p, bool a_kc, bool b_kc, bool vec, int cfg,
                     hipStream_t stream);
+// Convolution products with the image gathered by the loads (p.cg): mode 1
+// the forward (A = unfolded input, NT; K a multiple of 32), mode 2 the weight
+// gradient (B = unfolded input, TN). fp32, 16-byte loads and stores, on the
+// DMA tiles 256x256 (cfg 6) and 128x128 (cfg 10, 11) only.
+hipError_t gemm_f32_conv(const GemmParams& p, int mode, int cfg, hipStream_t stream);
+bool gemm_conv_cfg(int cfg);
 // bf16 operands (fp32 accumulation, bias and output). vec: 16-byte loads
 // (8 elements) and 16-byte stores; else 2-byte loads and 4-byte stores.
 hipError_t gemm_bf16(const GemmParams& p, bool a_kc, bool b_kc, bool vec, int cfg,

@@ -72,3 +72,42 @@ def test_conv_bwd_validation():
     assert b.lib.mt_conv2d_bwd_workspace(R(X), R(Wt), R(dY), R(dX), R(dW), R(dB), 1, 1, 1, 1,
                                          ctypes.byref(n)) == 0
     assert n.value >= 2 * 9 * 9 * 72 * 4
+
+
+def test_conv_gather_needs_no_unfolded_input():
+    """Channels-last x and w with C a multiple of 32: the forward product and
+    the weight gradient gather the image in their loads, so the forward needs
+    no workspace and a backward without dx none for the unfolded input. Other
+    layouts (or the gather switched off) keep the unfolded workspace."""
+    X = cl([2, 32, 9, 9], 0x1000000)
+    Wt = cl([16, 32, 3, 3], 0x2000000)
+    B = D([16], ptr=0x3000000)
+    Y = cl([2, 16, 9, 9], 0x4000000)
+    col = (2 * 9 * 9 * 288 * 4 + 255) // 256 * 256
+    n = ctypes.c_size_t(123)
+
+    def fwd_ws(x, w):
+        assert b.lib.mt_conv2d_fwd_workspace(R(x), R(w), R(B), R(Y), 1, 1, 1, 1, ctypes.byref(n)) == 0
+        return n.value
+
+    def bwd_ws(dx, dw, db):
+        assert b.lib.mt_conv2d_bwd_workspace(R(X), R(Wt), R(Y), R(dx), R(dw), R(db), 1, 1, 1, 1,
+                                             ctypes.byref(n)) == 0
+        return n.value
+
+    dX = cl([2, 32, 9, 9], 0x5000000)
+    dW = cl([16, 32, 3, 3], 0x6000000)
+    try:
+        assert fwd_ws(X, Wt) == 0
+        assert fwd(X, Wt, B, Y, st=(0, 1)) == 9        # still validated first
+        assert fwd_ws(X, D([16, 32, 3, 3], ptr=0x2000000)) == col   # [CO][C][KH][KW] weights
+        assert fwd_ws(D([2, 32, 9, 9], ptr=0x1000000), Wt) == col   # [N][C][H][W] input
+        assert fwd_ws(cl([2, 32, 9, 9], 0x1000004), Wt) == col      # x not 16-byte aligned
+        assert bwd_ws(None, dW, None) < col                          # dW gathers: partials only
+        assert bwd_ws(dX, dW, None) >= col                           # dU for dx
+        assert b.lib.mt_debug_set(b"conv_gather", 0) == 0
+        assert fwd_ws(X, Wt) == col
+        assert bwd_ws(None, dW, None) >= col
+    finally:
+        b.lib.mt_debug_set(b"conv_gather", 1)
+    assert b.lib.mt_debug_set(b"conv_gather", 2) == -2

@@ -187,3 +187,78 @@ def test_conv2d_backward_reuses_the_forward_unfold():
     b.conv2d_bwd(xd, wd, dyd, dx, dw, db, st, pd, workspace=ws, reuse_unfold=True)
     torch.cuda.synchronize()
     check(case, x, w, bias, dy, y, dx, dw, db)
+
+
+# Layouts where the products gather the image in their loads (channels-last x
+# and w; the forward needs C % 32 == 0, the weight gradient C % 4 == 0):
+# strides, paddings, 1x1 to 7x7 windows, several images per 256-pixel tile,
+# ragged last tiles, CO not a multiple of the tile.
+GATHER_CASES = [
+    (2, 32, 7, 6, 16, 3, 3, (1, 1), (1, 1), "cl", "cl"),
+    (3, 64, 9, 11, 20, 3, 3, (2, 2), (1, 1), "cl", "cl"),
+    (1, 32, 5, 5, 8, 5, 5, (1, 1), (0, 0), "cl", "cl"),
+    (2, 96, 8, 8, 36, 1, 1, (1, 1), (0, 0), "cl", "cl"),
+    (2, 32, 10, 7, 12, 5, 3, (2, 1), (2, 0), "cl", "cl"),
+    (2, 64, 6, 6, 64, 7, 7, (3, 3), (3, 3), "cl", "cl"),
+    (2, 12, 11, 13, 20, 2, 4, (3, 2), (0, 1), "cl", "cl"),
+    (5, 32, 20, 20, 40, 3, 3, (1, 1), (1, 1), "cl", "cl"),
+]
+
+
+@pytest.mark.parametrize("cfg", [-1, 5, 6, 10, 11])
+@pytest.mark.parametrize("case", GATHER_CASES, ids=[f"g{i}" for i in range(len(GATHER_CASES))])
+def test_conv2d_gather_parity(case, cfg):
+    """The gathering products against the oracle; with one of their tiles
+    forced (6: 256x256, 10 / 11: 128x128), also bit-identical to the same
+    tile reading the unfolded input (the same values reach LDS in the same
+    order). A forced tile outside that set (5) maps to 128x128."""
+    x, w, bias, dy = make(case, seed=31)
+    try:
+        b.debug_set("cfg", cfg)
+        got = run(case, x, w, bias, dy)
+        check(case, x, w, bias, dy, *got)
+        if cfg in (6, 10, 11):
+            b.debug_set("conv_gather", 0)
+            ref = run(case, x, w, bias, dy)
+            check(case, x, w, bias, dy, *ref)
+            for a, r, name in zip(got, ref, ("y", "dx", "dw", "db")):
+                d = (a - r).abs()
+                assert torch.equal(a, r), (f"{name}: gathered and unfolded products differ: max "
+                                           f"{float(d.max())} at {int(d.argmax())}, "
+                                           f"{int((d > 0).sum())} of {d.numel()}")
+    finally:
+        b.debug_set("conv_gather", 1)
+        b.debug_set("cfg", -1)
+
+
+def test_conv2d_gather_split_weight_gradient():
+    """A long pixel contraction split into runs (dW), with the pixel count not
+    a multiple of the 32-pixel stage."""
+    case = (7, 32, 30, 29, 32, 3, 3, (1, 1), (1, 1), "cl", "cl")
+    x, w, bias, dy = make(case, seed=37)
+    try:
+        b.debug_set("splits", 5)
+        got = run(case, x, w, bias, dy, outputs=("dw",))
+    finally:
+        b.debug_set("splits", 0)
+    check(case, x, w, bias, dy, *got)
+
+
+def test_conv2d_reuse_flag_after_a_gathering_forward():
+    """The forward gathered (no unfolded input left in the workspace) and the
+    weight gradient cannot (dw 4 bytes off 16-byte alignment): the backward
+    unfolds by itself although MT_CONV_REUSE_UNFOLD is passed."""
+    case = (2, 32, 9, 9, 16, 3, 3, (1, 1), (1, 1), "cl", "cl")
+    x, w, bias, dy = make(case, seed=41)
+    N, C, H, W, CO, KH, KW, st, pd, wlay, xlay = case
+    xd, wd, bd, dyd = to_dev(x, xlay), to_dev(w, wlay), bias.to(DEV), to_dev(dy, "cl")
+    y = torch.empty(N, CO, 9, 9, device=DEV).contiguous(memory_format=CL)
+    assert b.conv2d_fwd_workspace(xd, wd, bd, y, st, pd) == 0
+    b.conv2d_fwd(xd, wd, bd, y, st, pd)
+    store = torch.full((CO * KH * KW * C + 1,), float("nan"), device=DEV)
+    dw = store[1:].view(CO, KH, KW, C).permute(0, 3, 1, 2)
+    n = b.conv2d_bwd_workspace(xd, wd, dyd, None, dw, None, st, pd)
+    ws = torch.full((n // 4 + 64,), float("nan"), device=DEV)
+    b.conv2d_bwd(xd, wd, dyd, None, dw, None, st, pd, workspace=ws, reuse_unfold=True)
+    torch.cuda.synchronize()
+    check(case, x, w, bias, dy, y, None, dw, None)
