@@ -233,8 +233,10 @@ mt_status mt_rmsprop_step(int32_t n, const mt_tensor* params, const mt_tensor* g
  * (the forward's workspace size is then 0). Otherwise U is unfolded into the
  * caller's workspace, which is REQUIRED for that path (MT_ERR_WORKSPACE
  * without it; size from the *_workspace call: N Ho Wo x round_up(C KH KW, 4)
- * floats, plus split-K partials for dw). The backward's dx always goes through
- * dU = dY Wf in the workspace. fp32 only.
+ * floats, plus split-K partials for dw). The backward's dx is one product
+ * gathering dy where the convolution has stride 1, CO is a multiple of 32 and
+ * dx is channels-last (16-byte aligned); otherwise it goes through dU = dY Wf
+ * in the workspace and a fold. fp32 only.
  */
 mt_status mt_conv2d_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* b,
                         const mt_tensor* y, int32_t stride_h, int32_t stride_w, int32_t pad_h,

@@ -889,6 +889,43 @@ bool conv_gather(const ConvPlan& cp, const mt_tensor* x, int mode, mt::ConvGathe
   return true;
 }
 
+// Whether the input gradient of a stride-1 convolution may run as one product
+// gathering dY (dx = V W with V[(n, h, w)][(u, v, co)] = dY[n][h + ph - u][w + pw - v][co]
+// and W read tap by tap) instead of dU = dY Wf and the fold: channels-last
+// dy, w and dx, CO a multiple of 32, 16-byte aligned rows. The description
+// reuses the forward's fields with the roles turned round: the gathered image
+// is dy (CO channels, HO x WO), rows decode over H x W, and the window origin
+// is h + ph (taps enter with a minus sign).
+bool conv_dgrad_gather(const ConvPlan& cp, const mt_tensor* dy, const mt_tensor* w,
+                       const mt_tensor* dx, mt::ConvGather* cg) {
+  const mt::ConvGeom& g = cp.g;
+  if (!g_conv_gather || g_force_vec1 || !g.korder_uvc || g.sh != 1 || g.sw != 1) return false;
+  if (g.CO % 32 != 0 || g.C % 4 != 0 || !channels_last(dx) || !aligned16(dx->data)) return false;
+  if (!aligned16(dy->data) || !aligned16(w->data) || cp.wpitch % 4 != 0) return false;
+  const int64_t lim = (int64_t)1 << 14;
+  if (g.H >= lim || g.W >= lim || g.HO >= lim || g.WO >= lim || g.KH >= lim || g.KW >= lim ||
+      g.ph >= lim || g.pw >= lim)
+    return false;
+  const int64_t ys0 = dy->stride[0], ys2 = dy->stride[2], ys3 = dy->stride[3];
+  if (ys0 % 4 || ys2 % 4 || ys3 % 4) return false;
+  const int64_t ext = (int64_t)(g.N - 1) * ys0 + (int64_t)(g.HO - 1) * ys2 +
+                      (int64_t)(g.WO - 1) * ys3 + g.CO;
+  if ((int64_t)g.N * ys0 + (int64_t)(g.H + g.ph + 1) * ys2 + (int64_t)(g.W + g.pw + 1) * ys3 +
+          g.CO >= ((int64_t)1 << 29))
+    return false;
+  if ((int64_t)g.N * g.H * g.W >= ((int64_t)1 << 31) - 64) return false;
+  std::memset(cg, 0, sizeof(*cg));
+  cg->x = (const float*)dy->data;
+  cg->x_bytes = (uint32_t)(ext * 4);
+  cg->C = g.CO; cg->H = g.HO; cg->W = g.WO; cg->KW = g.KW;
+  cg->sh = 1; cg->sw = 1; cg->ph = -g.ph; cg->pw = -g.pw;
+  cg->HO = g.H; cg->WO = g.W;
+  cg->xs0 = (int32_t)ys0; cg->xs2 = (int32_t)ys2; cg->xs3 = (int32_t)ys3;
+  fast_div_params(g.W, &cg->wo_mag, &cg->wo_shift);
+  fast_div_params(g.H, &cg->ho_mag, &cg->ho_shift);
+  return true;
+}
+
 mt_status check_act4(const mt_tensor* t, const char* name, int64_t N, int64_t C, int64_t H,
                      int64_t W) {
   mt_status s = check_tensor(t, name, 4, 4);
@@ -1032,9 +1069,11 @@ mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
     parts = g_force_parts > 0 ? g_force_parts : mt::colsum_parts(cp.M, g.CO);
     if (parts > 1) need_db = (size_t)parts * g.CO * sizeof(float);
   }
-  // the unfolded matrix (U for an unfolded dW, then dU for dx) heads the
-  // workspace, the split partials follow
-  const size_t col_need = (dx || (dw && !gdw.conv)) ? cp.col_bytes : 0;
+  mt::ConvGather dcg;
+  const bool dx_gather = dx && conv_dgrad_gather(cp, dy, w, dx, &dcg);
+  // the unfolded matrix (U for an unfolded dW, then dU for an unfolded dx)
+  // heads the workspace, the split partials follow
+  const size_t col_need = ((dx && !dx_gather) || (dw && !gdw.conv)) ? cp.col_bytes : 0;
   const size_t need = col_need + std::max(need_dw, need_db);
   if (ws_query) {
     *ws_query = need;
@@ -1068,7 +1107,29 @@ mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
                                    parts, stream))))
       return s;
   }
-  if (dx && cp.M > 0) {
+  if (dx && dx_gather && cp.M > 0) {
+    // dx = V W in one product, V gathered from dy; dx's rows are input pixels
+    GemmCall gdx{};
+    init_params(&gdx.p);
+    gdx.p.a = dy->data;
+    gdx.p.b = w->data;
+    gdx.p.c = (float*)dx->data;
+    gdx.p.M = (int64_t)g.N * g.H * g.W;
+    gdx.p.N = g.C;
+    gdx.p.K = (int64_t)g.KH * g.KW * g.CO;  // k = (u, v, co)
+    gdx.p.lda = 0;
+    gdx.p.ldb = cp.wpitch;
+    gdx.p.ldc = g.C;
+    gdx.p.accumulate = acc;
+    gdx.p.cg = dcg;
+    gdx.a_kc = true;
+    gdx.b_kc = false;
+    gdx.bf16 = false;
+    gdx.vec = true;
+    gdx.cfg = -1;
+    gdx.conv = 3;
+    if ((s = launch_gemm(gdx, stream, nullptr, 0))) return s;
+  } else if (dx && cp.M > 0) {
     // dU = dY Wf into the workspace (U is no longer needed), then the fold
     GemmCall gdx{};
     init_params(&gdx.p);

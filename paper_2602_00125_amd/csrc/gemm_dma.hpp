@@ -455,14 +455,16 @@ void gemm_dma_kernel(const GemmParams p) {
 #include "gemm_dma_body.inc"
 }
 
-// The convolution products with the image gathered by the loads: CONV_ 1 the
-// forward (y = U Wf^T + b, NT), 2 the weight gradient (dW = dY^T U, TN).
+// The convolution products with an operand gathered by the loads: CONV_ 1 the
+// forward (y = U Wf^T + b, NT), 2 the weight gradient (dW = dY^T U, TN), 3
+// the input gradient of a stride-1 convolution (dx = V W, NN, V gathered from
+// dY: V[(n, h, w)][(u, v, co)] = dY[n][h + ph - u][w + pw - v][co]).
 template <int CONV_, int BM, int BN, int BK, int WGM, int WGN, int NS, bool KTAIL, int WAVES_PER_EU>
 __global__ __launch_bounds__(WGM * WGN * 64)
 __attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
 void conv_dma_kernel(const GemmParams p) {
   using T = float;
-  constexpr bool A_KC = CONV_ == 1, B_KC = CONV_ == 1, EPI = false, VEC_C = true;
+  constexpr bool A_KC = CONV_ != 2, B_KC = CONV_ == 1, EPI = false, VEC_C = true;
   constexpr int DMA_G0 = 1, DMA_GS = 1, DMA_LANE = 16, CONV = CONV_;
 #include "gemm_dma_body.inc"
 }

@@ -122,8 +122,8 @@ static hipError_t launch_conv(const GemmParams& p, hipStream_t stream) {
   if (blocks <= 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   if (p.K % BK != 0) {
-    // the forward's stages are whole channel groups of one tap
-    if constexpr (MODE == 1) return hipErrorInvalidValue;
+    // the forward's and the input gradient's stages are whole channel groups of one tap
+    if constexpr (MODE != 2) return hipErrorInvalidValue;
     else
       hipLaunchKernelGGL((gemm::conv_dma_kernel<MODE, BM, BN, BK, WGM, WGN, NS, true, WPE>),
                          dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, stream, q);
@@ -151,6 +151,7 @@ bool gemm_conv_cfg(int cfg) {
 hipError_t gemm_f32_conv(const GemmParams& p, int mode, int cfg, hipStream_t stream) {
   if (mode == 1) return conv_cfg<1>(p, cfg, stream);
   if (mode == 2) return conv_cfg<2>(p, cfg, stream);
+  if (mode == 3) return conv_cfg<3>(p, cfg, stream);
   return hipErrorInvalidValue;
 }
 

@@ -35,9 +35,11 @@ int gemm_tile_k(int cfg, bool bf16);
 // contiguous extent, pitch, batch stride and base allows them); else 4-byte.
 hipError_t gemm_f32(const GemmParams& p, bool a_kc, bool b_kc, bool vec, int cfg,
                     hipStream_t stream);
-// Convolution products with the image gathered by the loads (p.cg): mode 1
+// Convolution products with an operand gathered by the loads (p.cg): mode 1
 // the forward (A = unfolded input, NT; K a multiple of 32), mode 2 the weight
-// gradient (B = unfolded input, TN). fp32, 16-byte loads and stores, on the
+// gradient (B = unfolded input, TN), mode 3 the input gradient of a stride-1
+// convolution (A = dY unfolded over the mirrored taps, B = the weights tap by
+// tap, NN; K a multiple of 32). fp32, 16-byte loads and stores, on the
 // DMA tiles 256x256 (cfg 6) and 128x128 (cfg 10, 11) only.
 hipError_t gemm_f32_conv(const GemmParams& p, int mode, int cfg, hipStream_t stream);
 bool gemm_conv_cfg(int cfg);

@@ -104,7 +104,17 @@ def test_conv_gather_needs_no_unfolded_input():
         assert fwd_ws(D([2, 32, 9, 9], ptr=0x1000000), Wt) == col   # [N][C][H][W] input
         assert fwd_ws(cl([2, 32, 9, 9], 0x1000004), Wt) == col      # x not 16-byte aligned
         assert bwd_ws(None, dW, None) < col                          # dW gathers: partials only
-        assert bwd_ws(dX, dW, None) >= col                           # dU for dx
+        assert bwd_ws(dX, dW, None) >= col                           # dU for dx (CO % 32 != 0)
+        # CO a multiple of 32 and stride 1: dx gathers dy as well, no dU
+        W32, dW32 = cl([32, 32, 3, 3], 0x2000000), cl([32, 32, 3, 3], 0x6000000)
+        dY32 = cl([2, 32, 9, 9], 0x4000000)
+        assert b.lib.mt_conv2d_bwd_workspace(R(X), R(W32), R(dY32), R(dX), R(dW32), None, 1, 1, 1, 1,
+                                             ctypes.byref(n)) == 0
+        assert n.value < col
+        dY5 = cl([2, 32, 5, 5], 0x4000000)
+        assert b.lib.mt_conv2d_bwd_workspace(R(X), R(W32), R(dY5), R(dX), R(dW32), None, 2, 2, 1, 1,
+                                             ctypes.byref(n)) == 0
+        assert n.value >= (2 * 5 * 5 * 288 * 4 + 255) // 256 * 256  # stride 2: dU and the fold
         assert b.lib.mt_debug_set(b"conv_gather", 0) == 0
         assert fwd_ws(X, Wt) == col
         assert bwd_ws(None, dW, None) >= col

@@ -189,10 +189,11 @@ def test_conv2d_backward_reuses_the_forward_unfold():
     check(case, x, w, bias, dy, y, dx, dw, db)
 
 
-# Layouts where the products gather the image in their loads (channels-last x
-# and w; the forward needs C % 32 == 0, the weight gradient C % 4 == 0):
-# strides, paddings, 1x1 to 7x7 windows, several images per 256-pixel tile,
-# ragged last tiles, CO not a multiple of the tile.
+# Layouts where the products gather an operand in their loads (channels-last
+# x and w; the forward needs C % 32 == 0, the weight gradient C % 4 == 0, the
+# input gradient stride 1 and CO % 32 == 0): strides, paddings, 1x1 to 7x7
+# windows, several images per 256-pixel tile, ragged last tiles, CO not a
+# multiple of the tile.
 GATHER_CASES = [
     (2, 32, 7, 6, 16, 3, 3, (1, 1), (1, 1), "cl", "cl"),
     (3, 64, 9, 11, 20, 3, 3, (2, 2), (1, 1), "cl", "cl"),
@@ -202,16 +203,24 @@ GATHER_CASES = [
     (2, 64, 6, 6, 64, 7, 7, (3, 3), (3, 3), "cl", "cl"),
     (2, 12, 11, 13, 20, 2, 4, (3, 2), (0, 1), "cl", "cl"),
     (5, 32, 20, 20, 40, 3, 3, (1, 1), (1, 1), "cl", "cl"),
+    (2, 32, 7, 6, 32, 3, 3, (1, 1), (1, 1), "cl", "cl"),
+    (3, 8, 9, 11, 64, 3, 3, (1, 1), (1, 1), "cl", "cl"),
+    (1, 12, 5, 5, 32, 5, 5, (1, 1), (0, 0), "cl", "cl"),
+    (2, 64, 6, 6, 64, 7, 7, (1, 1), (3, 3), "cl", "cl"),
+    (2, 4, 10, 7, 32, 5, 3, (1, 1), (2, 0), "cl", "cl"),
+    (3, 36, 17, 19, 96, 3, 3, (1, 1), (1, 1), "cl", "cl"),
 ]
 
 
 @pytest.mark.parametrize("cfg", [-1, 5, 6, 10, 11])
 @pytest.mark.parametrize("case", GATHER_CASES, ids=[f"g{i}" for i in range(len(GATHER_CASES))])
 def test_conv2d_gather_parity(case, cfg):
-    """The gathering products against the oracle; with one of their tiles
-    forced (6: 256x256, 10 / 11: 128x128), also bit-identical to the same
-    tile reading the unfolded input (the same values reach LDS in the same
-    order). A forced tile outside that set (5) maps to 128x128."""
+    """The gathering products against the oracle, and the unfolded path too;
+    with one of their tiles forced (6: 256x256, 10 / 11: 128x128), y and dw
+    also bit-identical to the same tile reading the unfolded input (the same
+    values reach LDS in the same order; dx sums in another order when
+    gathered: one product instead of dU and the fold). A forced tile outside
+    that set (5) maps to 128x128."""
     x, w, bias, dy = make(case, seed=31)
     try:
         b.debug_set("cfg", cfg)
@@ -222,6 +231,8 @@ def test_conv2d_gather_parity(case, cfg):
             ref = run(case, x, w, bias, dy)
             check(case, x, w, bias, dy, *ref)
             for a, r, name in zip(got, ref, ("y", "dx", "dw", "db")):
+                if name == "dx":
+                    continue
                 d = (a - r).abs()
                 assert torch.equal(a, r), (f"{name}: gathered and unfolded products differ: max "
                                            f"{float(d.max())} at {int(d.argmax())}, "
@@ -262,3 +273,36 @@ def test_conv2d_reuse_flag_after_a_gathering_forward():
     b.conv2d_bwd(xd, wd, dyd, None, dw, None, st, pd, workspace=ws, reuse_unfold=True)
     torch.cuda.synchronize()
     check(case, x, w, bias, dy, y, None, dw, None)
+
+
+def test_conv2d_gathered_input_gradient_accumulates():
+    """dx gathered from dy (stride 1, CO % 32 == 0) into channels-last dx with
+    MT_ACCUMULATE; an [N][C][H][W] dx takes the dU + fold path instead."""
+    case = (2, 16, 12, 10, 32, 3, 3, (1, 1), (1, 1), "cl", "cl")
+    x, w, bias, dy = make(case, seed=43)
+    N, C, H, W, CO, KH, KW = case[:7]
+    prior = (torch.randn(N, C, H, W, device=DEV), torch.randn(CO, C, KH, KW, device=DEV),
+             torch.randn(CO, device=DEV))
+    y, dx, dw, db = run(case, x, w, bias, dy, accumulate=True, prior=prior)
+    check(case, x, w, bias, dy, y, dx, dw, db, prior=prior)
+    y, dx, _, _ = run(case, x, w, bias, dy, outputs=("dx",), dx_layout="nchw")
+    check(case, x, w, bias, dy, y, dx, None, None)
+
+
+def test_conv2d_gathered_backward_needs_no_unfolded_workspace():
+    """Every product of the step gathers: the backward's workspace holds only
+    split partials, and the step runs with no workspace at all."""
+    case = (4, 32, 14, 14, 64, 3, 3, (1, 1), (1, 1), "cl", "cl")
+    x, w, bias, dy = make(case, seed=47)
+    N, C, H, W, CO, KH, KW, st, pd, wlay, xlay = case
+    xd, wd, bd, dyd = to_dev(x, xlay), to_dev(w, wlay), bias.to(DEV), to_dev(dy, "cl")
+    y = torch.empty(N, CO, H, W, device=DEV).contiguous(memory_format=CL)
+    dx = torch.empty(N, C, H, W, device=DEV).contiguous(memory_format=CL)
+    dw = torch.empty_like(wd)
+    db = torch.empty(CO, device=DEV)
+    col = N * H * W * C * KH * KW * 4
+    assert b.conv2d_bwd_workspace(xd, wd, dyd, dx, dw, db, st, pd) < col
+    b.conv2d_fwd(xd, wd, bd, y, st, pd)
+    b.conv2d_bwd(xd, wd, dyd, dx, dw, db, st, pd)
+    torch.cuda.synchronize()
+    check(case, x, w, bias, dy, y, dx, dw, db)
