@@ -229,11 +229,15 @@ mt_status mt_rmsprop_step(int32_t n, const mt_tensor* params, const mt_tensor* g
  * Where x is channels-last (c stride 1, the other strides multiples of 4, a
  * 16-byte aligned base), w is channels-last and C is a multiple of 32 (the
  * weight gradient: of 4), with y, w and b allowing 16-byte accesses, the
- * product's loads gather U's entries from x directly and U is never formed
- * (the forward's workspace size is then 0). Otherwise U is unfolded into the
- * caller's workspace, which is REQUIRED for that path (MT_ERR_WORKSPACE
- * without it; size from the *_workspace call: N Ho Wo x round_up(C KH KW, 4)
- * floats, plus split-K partials for dw). The backward's dx is one product
+ * product's loads gather U's entries from x directly and U is never formed.
+ * Otherwise U is unfolded into the caller's workspace, which is REQUIRED for
+ * that path (MT_ERR_WORKSPACE without it; N Ho Wo x round_up(C KH KW, 4)
+ * floats at its start). After U (or from the start) the workspace holds the
+ * partial tiles of a split contraction or of the stream-K schedule (the
+ * tile-major K-stages shared evenly by one block per CU, cut tiles summed by
+ * a fixed-order pass) that products with a ragged last wave of tiles take;
+ * those are optional: a shorter workspace runs one tile per block. Sizes
+ * from the *_workspace calls. The backward's dx is one product
  * gathering dy where the convolution has stride 1, CO is a multiple of 32 and
  * dx is channels-last (16-byte aligned); otherwise it goes through dU = dY Wf
  * in the workspace and a fold. fp32 only.

@@ -27,6 +27,8 @@ int g_force_splits = 0;
 int g_force_parts = 0;
 int g_krot = 1;  // K-stage rotation per XCD in the DMA kernel (measured: bf16 NT +2%, others neutral)
 int g_conv_gather = 1;  // convolution products gather the image where the layout allows
+int g_stream_k = 1;     // gathered 256x256 convolution products: 0 never, 1 on a ragged last wave, 2 always
+int g_sk_blocks = 0;    // stream-K blocks (0: one per CU, 256)
 
 mt_status fail(mt_status s, const std::string& msg) {
   g_err = msg;
@@ -207,7 +209,8 @@ struct GemmCall {
   bool vec;   // 16-byte operand loads and output stores
   bool bf16;  // bf16 operands (else fp32)
   int cfg;
-  int conv;   // 1 / 2: A / B gathered from the image (p.cg), else 0
+  int conv;   // 1 / 2 / 3: the convolution product gathering an operand (p.cg), else 0
+  int sk;     // stream-K blocks (conv 1 and 3 on the 256x256 tile), else 0
 };
 
 // Whether an operand allows 16-byte loads: `per` elements per vector (4 fp32,
@@ -255,7 +258,24 @@ size_t plan_gemm(GemmCall& g, bool may_split) {
   p.stages_per_split = stages > 0 ? stages : 1;
   p.partial = nullptr;
   p.partial_stride = 0;
+  g.sk = 0;
   if (!may_split || p.M == 0 || p.N == 0 || p.keep_count == 0 || stages == 0) return 0;
+  // The gathered forward / input-gradient products on the 256x256 tile (one
+  // block per CU) whose tiles leave the last wave under 90% full: stream-K,
+  // every CU taking an equal share of the tile-major K-stages (at least
+  // kDmaMinRunStages each); cut tiles are summed by a finish pass
+  if ((g.conv == 1 || g.conv == 3) && g.cfg == mt::kCfgDma256x256 && g_stream_k) {
+    const int64_t G = g_sk_blocks > 0 ? g_sk_blocks : 256;
+    const int64_t T = cdiv(p.M, 256) * cdiv(p.N, 256);
+    const bool ragged = T > G && (double)T / (double)(cdiv(T, G) * G) < 0.9 &&
+                        T * stages >= G * kDmaMinRunStages;
+    // (at least one stage per block keeps the block boundaries distinct)
+    if ((g_stream_k == 2 && T * stages >= G) || ragged) {
+      g.sk = (int)G;
+      p.partial_stride = p.M * p.N;
+      return (size_t)mt::sk_max_segments(T, stages, G) * p.M * p.N * sizeof(float);
+    }
+  }
   const int64_t blocks = cdiv(p.M, mt::gemm_tile_m(g.cfg)) * cdiv(p.N, mt::gemm_tile_n(g.cfg)) *
                          p.keep_count;
   const int want = choose_splits(blocks, stages, g.cfg);
@@ -273,7 +293,10 @@ mt_status launch_gemm(GemmCall& g, hipStream_t stream, void* ws, size_t ws_bytes
   mt::GemmParams& p = g.p;
   if (p.M == 0 || p.N == 0 || p.keep_count == 0) return MT_OK;
   const size_t need = plan_gemm(g, ws != nullptr);
-  if (need > 0 && need <= ws_bytes) {
+  if (g.sk && need > ws_bytes) g.sk = 0;  // no room for the partial tiles: one tile per block
+  if (g.sk) {
+    p.partial = (float*)ws;
+  } else if (need > 0 && need <= ws_bytes) {
     p.partial = (float*)ws;
   } else {
     p.splits = 1;
@@ -287,6 +310,7 @@ mt_status launch_gemm(GemmCall& g, hipStream_t stream, void* ws, size_t ws_bytes
   if (rows_a * p.lda * es >= (int64_t)1 << 31 || rows_b * p.ldb * es >= (int64_t)1 << 31)
     return fail(MT_ERR_LAYOUT, "row pitch too large for 32-bit tile offsets");
   (void)hipGetLastError();  // clear a stale error so the launch check is ours
+  if (g.sk) return hip_status(mt::gemm_f32_conv_sk(p, g.conv, g.sk, stream));
   hipError_t e = g.conv   ? mt::gemm_f32_conv(p, g.conv, g.cfg, stream)
                  : g.bf16 ? mt::gemm_bf16(p, g.a_kc, g.b_kc, g.vec, g.cfg, stream)
                           : mt::gemm_f32(p, g.a_kc, g.b_kc, g.vec, g.cfg, stream);
@@ -968,25 +992,33 @@ mt_status conv_fwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
   // the product reads the image itself where it can, else the unfolded input
   // in the workspace
   const bool gather = gc.vec && conv_gather(cp, x, 1, &gc.p.cg);
-  if (ws_query) {
-    *ws_query = gather ? 0 : cp.col_bytes;
-    return MT_OK;
-  }
-  if (cp.M == 0) return MT_OK;
   if (gather) {
     gc.conv = 1;
     gc.p.a = x->data;
     gc.p.lda = 0;
-    return launch_gemm(gc, stream, nullptr, 0);
   }
-  if (!ws || ws_bytes < cp.col_bytes || ((uintptr_t)ws & 255))
+  // the workspace: the unfolded input (if the product does not gather), then
+  // split-K or stream-K partial tiles (optional: without them one tile per
+  // block over the whole contraction)
+  const size_t col_need = gather ? 0 : cp.col_bytes;
+  if (ws_query) {
+    GemmCall probe = gc;
+    *ws_query = col_need + plan_gemm(probe, true);
+    return MT_OK;
+  }
+  if (cp.M == 0) return MT_OK;
+  if (ws && ((uintptr_t)ws & 255)) return fail(MT_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (!gather && (!ws || ws_bytes < cp.col_bytes))
     return fail(MT_ERR_WORKSPACE, "convolution: needs a 256-byte aligned workspace of "
                                   "mt_conv2d_fwd_workspace bytes (the unfolded input)");
-  float* col = (float*)ws;
-  (void)hipGetLastError();
-  if ((s = hip_status(mt::conv_unfold((const float*)x->data, g, col, stream)))) return s;
-  gc.p.a = col;
-  return launch_gemm(gc, stream, nullptr, 0);
+  char* rest = ws ? (char*)ws + col_need : nullptr;
+  const size_t rest_bytes = ws && ws_bytes > col_need ? ws_bytes - col_need : 0;
+  if (!gather) {
+    (void)hipGetLastError();
+    if ((s = hip_status(mt::conv_unfold((const float*)x->data, g, (float*)ws, stream)))) return s;
+    gc.p.a = ws;
+  }
+  return launch_gemm(gc, stream, rest_bytes ? rest : nullptr, rest_bytes);
 }
 
 mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor* dy,
@@ -1069,12 +1101,39 @@ mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
     parts = g_force_parts > 0 ? g_force_parts : mt::colsum_parts(cp.M, g.CO);
     if (parts > 1) need_db = (size_t)parts * g.CO * sizeof(float);
   }
-  mt::ConvGather dcg;
-  const bool dx_gather = dx && conv_dgrad_gather(cp, dy, w, dx, &dcg);
+  // dx = V W in one product where dy can be gathered (V: dy over the
+  // mirrored taps), its rows the input pixels
+  GemmCall gdxg{};
+  const bool dx_gather = dx && conv_dgrad_gather(cp, dy, w, dx, &gdxg.p.cg);
+  size_t need_dx = 0;
+  if (dx_gather) {
+    const mt::ConvGather dcg = gdxg.p.cg;
+    init_params(&gdxg.p);
+    gdxg.p.cg = dcg;
+    gdxg.p.a = dy->data;
+    gdxg.p.b = w->data;
+    gdxg.p.c = (float*)dx->data;
+    gdxg.p.M = (int64_t)g.N * g.H * g.W;
+    gdxg.p.N = g.C;
+    gdxg.p.K = (int64_t)g.KH * g.KW * g.CO;  // k = (u, v, co)
+    gdxg.p.lda = 0;
+    gdxg.p.ldb = cp.wpitch;
+    gdxg.p.ldc = g.C;
+    gdxg.p.accumulate = acc;
+    gdxg.a_kc = true;
+    gdxg.b_kc = false;
+    gdxg.bf16 = false;
+    gdxg.vec = true;
+    gdxg.cfg = -1;
+    gdxg.conv = 3;
+    GemmCall probe = gdxg;
+    need_dx = plan_gemm(probe, true);
+  }
   // the unfolded matrix (U for an unfolded dW, then dU for an unfolded dx)
-  // heads the workspace, the split partials follow
+  // heads the workspace; split or stream-K partials follow (the products run
+  // one after another and share them)
   const size_t col_need = ((dx && !dx_gather) || (dw && !gdw.conv)) ? cp.col_bytes : 0;
-  const size_t need = col_need + std::max(need_dw, need_db);
+  const size_t need = col_need + std::max(std::max(need_dw, need_db), need_dx);
   if (ws_query) {
     *ws_query = need;
     return MT_OK;
@@ -1108,27 +1167,7 @@ mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
       return s;
   }
   if (dx && dx_gather && cp.M > 0) {
-    // dx = V W in one product, V gathered from dy; dx's rows are input pixels
-    GemmCall gdx{};
-    init_params(&gdx.p);
-    gdx.p.a = dy->data;
-    gdx.p.b = w->data;
-    gdx.p.c = (float*)dx->data;
-    gdx.p.M = (int64_t)g.N * g.H * g.W;
-    gdx.p.N = g.C;
-    gdx.p.K = (int64_t)g.KH * g.KW * g.CO;  // k = (u, v, co)
-    gdx.p.lda = 0;
-    gdx.p.ldb = cp.wpitch;
-    gdx.p.ldc = g.C;
-    gdx.p.accumulate = acc;
-    gdx.p.cg = dcg;
-    gdx.a_kc = true;
-    gdx.b_kc = false;
-    gdx.bf16 = false;
-    gdx.vec = true;
-    gdx.cfg = -1;
-    gdx.conv = 3;
-    if ((s = launch_gemm(gdx, stream, nullptr, 0))) return s;
+    if ((s = launch_gemm(gdxg, stream, rest_bytes ? rest : nullptr, rest_bytes))) return s;
   } else if (dx && cp.M > 0) {
     // dU = dY Wf into the workspace (U is no longer needed), then the fold
     GemmCall gdx{};
@@ -1450,6 +1489,12 @@ int mt_debug_set(const char* key, int64_t value) {
   } else if (!std::strcmp(key, "conv_gather")) {
     if (value < 0 || value > 1) return -2;
     g_conv_gather = (int)value;
+  } else if (!std::strcmp(key, "stream_k")) {
+    if (value < 0 || value > 2) return -2;
+    g_stream_k = (int)value;
+  } else if (!std::strcmp(key, "sk_blocks")) {
+    if (value < 0 || value > 65535) return -2;
+    g_sk_blocks = (int)value;
   } else if (!std::strcmp(key, "splits") || !std::strcmp(key, "parts")) {
     if (value < 0 || value > 4096) return -2;
     (key[0] == 's' ? g_force_splits : g_force_parts) = (int)value;

@@ -452,6 +452,9 @@ __global__ __launch_bounds__(WGM * WGN * 64)
 __attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
 void gemm_dma_kernel(const GemmParams p) {
   constexpr int CONV = 0;
+  constexpr bool SK = false, sk_part = false;
+  constexpr int64_t sk_t = 0, sk_ka = 0, sk_kb = 0;
+  constexpr int sk_slot = 0;
 #include "gemm_dma_body.inc"
 }
 
@@ -466,7 +469,60 @@ void conv_dma_kernel(const GemmParams p) {
   using T = float;
   constexpr bool A_KC = CONV_ != 2, B_KC = CONV_ == 1, EPI = false, VEC_C = true;
   constexpr int DMA_G0 = 1, DMA_GS = 1, DMA_LANE = 16, CONV = CONV_;
+  constexpr bool SK = false, sk_part = false;
+  constexpr int64_t sk_t = 0, sk_ka = 0, sk_kb = 0;
+  constexpr int sk_slot = 0;
 #include "gemm_dma_body.inc"
+}
+
+// Stream-K schedule of the U = T KS K-stages of T tiles (tile-major, KS
+// stages each) over G blocks: block b takes stages [b U / G, (b+1) U / G).
+// A tile cut by block boundaries is summed in segments; sk_count(X) counts
+// the boundaries floor(b U / G) (b >= 0) below X, for X >= 1. With U >= G
+// the boundaries are distinct, so segments and boundaries match one to one.
+__host__ __device__ inline int64_t sk_count(int64_t X, int64_t G, int64_t U) {
+  return (X * G + U - 1) / U;
+}
+struct SkSeg {
+  int n;     // segments of the tile
+  int slot;  // index of the segment that starts at stage ka of the tile
+};
+__host__ __device__ inline SkSeg sk_segment(int64_t t, int64_t ka, int64_t KS, int64_t G,
+                                            int64_t U) {
+  const int64_t L = t * KS;
+  const int64_t c0 = sk_count(L + 1, G, U);
+  return {(int)(sk_count(L + KS, G, U) - c0 + 1), (int)(sk_count(L + ka + 1, G, U) - c0)};
+}
+
+// The stream-K form of the gathered forward (CONV_ 1) and input-gradient
+// (CONV_ 3) products, for grids that would leave a partial last wave of
+// tiles: every block (one per CU) computes its share of stages tile by tile;
+// a tile computed whole is written with its bias, the segments of a cut
+// tile go to partial slot `segment index` (p.partial, M x N each) and
+// sk_finish adds them in slot order. No block waits on another.
+template <int CONV_, int BM, int BN, int BK, int WGM, int WGN, int NS, int WAVES_PER_EU>
+__global__ __launch_bounds__(WGM * WGN * 64)
+__attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
+void conv_dma_sk_kernel(const GemmParams p) {
+  static_assert(CONV_ == 1 || CONV_ == 3, "stream-K: the gathered NT / NN products");
+  using T = float;
+  constexpr bool A_KC = true, B_KC = CONV_ == 1, EPI = false, VEC_C = true, KTAIL = false;
+  constexpr int DMA_G0 = 1, DMA_GS = 1, DMA_LANE = 16, CONV = CONV_;
+  constexpr bool SK = true;
+  const int64_t ks_all = (p.K + BK - 1) / BK;
+  const int64_t U = (int64_t)p.tiles_m * p.tiles_n * ks_all, G = gridDim.x;
+  const int64_t u_end = ((int64_t)blockIdx.x + 1) * U / G;
+  for (int64_t u = (int64_t)blockIdx.x * U / G; u < u_end;) {
+    const int64_t sk_t = u / ks_all;
+    const int64_t sk_ka = u - sk_t * ks_all;
+    const int64_t sk_kb = (u_end - sk_t * ks_all) < ks_all ? (u_end - sk_t * ks_all) : ks_all;
+    const SkSeg seg = sk_segment(sk_t, sk_ka, ks_all, G, U);
+    const bool sk_part = seg.n > 1;
+    const int sk_slot = seg.slot;
+#include "gemm_dma_body.inc"
+    u = sk_t * ks_all + sk_kb;
+    __syncthreads();  // the next segment's loads reuse the ring
+  }
 }
 
 }  // namespace gemm

@@ -144,6 +144,66 @@ static hipError_t conv_cfg(const GemmParams& p, int cfg, hipStream_t stream) {
   }
 }
 
+// Sum of the segments of every tile the stream-K product cut: C = sum over
+// slots s < n(t) of partial[s] (+ bias, + C), slots in order; tiles computed
+// whole were written by the product. A lane per 4 consecutive columns.
+__global__ __launch_bounds__(256) void sk_finish_kernel(const GemmParams p, int64_t G, int BM,
+                                                        int BN) {
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  const int64_t n4 = p.N / 4;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= p.M * n4) return;
+  const int64_t m = i / n4, n = (i - m * n4) * 4;
+  const int64_t ks = (p.K + 31) / 32;
+  const int64_t U = (int64_t)p.tiles_m * p.tiles_n * ks;
+  const int64_t t = (m / BM) * p.tiles_n + n / BN;
+  const gemm::SkSeg sg = gemm::sk_segment(t, 0, ks, G, U);
+  if (sg.n <= 1) return;
+  const float* src = p.partial + m * p.N + n;
+  f32x4 v = *(const f32x4*)src;
+  for (int s = 1; s < sg.n; ++s) v += *(const f32x4*)(src + s * p.partial_stride);
+  float* c = p.c + m * p.ldc + n;
+  if (p.bias) v += *(const f32x4*)(p.bias + n);
+  if (p.accumulate) v += *(const f32x4*)c;
+  *(f32x4*)c = v;
+}
+
+// Stream-K launch of the gathered forward / input-gradient product on the
+// 256x256 tile: G blocks, then the finish. The host has sized p.partial for
+// the most segments any tile gets (sk_max_segments).
+hipError_t gemm_f32_conv_sk(const GemmParams& p, int mode, int blocks, hipStream_t stream) {
+  GemmParams q = p;
+  q.tiles_m = (int32_t)((p.M + 255) / 256);
+  q.tiles_n = (int32_t)((p.N + 255) / 256);
+  if (p.M <= 0 || p.N <= 0 || blocks <= 0 || p.K % 32 != 0 || p.N % 4 != 0)
+    return hipErrorInvalidValue;
+  if (mode == 1)
+    hipLaunchKernelGGL((gemm::conv_dma_sk_kernel<1, 256, 256, 32, 2, 4, 2, 2>), dim3(blocks),
+                       dim3(512), 0, stream, q);
+  else if (mode == 3)
+    hipLaunchKernelGGL((gemm::conv_dma_sk_kernel<3, 256, 256, 32, 2, 4, 2, 2>), dim3(blocks),
+                       dim3(512), 0, stream, q);
+  else
+    return hipErrorInvalidValue;
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t groups = p.M * (p.N / 4);
+  if ((groups + 255) / 256 > 0x7fffffff) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL(sk_finish_kernel, dim3((unsigned)((groups + 255) / 256)), dim3(256), 0, stream,
+                     q, (int64_t)blocks, 256, 256);
+  return hipGetLastError();
+}
+
+int64_t sk_max_segments(int64_t tiles, int64_t ks, int64_t blocks) {
+  const int64_t U = tiles * ks;
+  int64_t most = 1;
+  for (int64_t t = 0; t < tiles; ++t) {
+    const int64_t n = gemm::sk_segment(t, 0, ks, blocks, U).n;
+    if (n > most) most = n;
+  }
+  return most;
+}
+
 bool gemm_conv_cfg(int cfg) {
   return cfg == kCfgDma256x256 || cfg == kCfgDma128x128 || cfg == kCfgDma128x128w8;
 }

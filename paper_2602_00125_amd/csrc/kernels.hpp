@@ -42,6 +42,11 @@ hipError_t gemm_f32(const GemmParams& p, bool a_kc, bool b_kc, bool vec, int cfg
 // tap, NN; K a multiple of 32). fp32, 16-byte loads and stores, on the
 // DMA tiles 256x256 (cfg 6) and 128x128 (cfg 10, 11) only.
 hipError_t gemm_f32_conv(const GemmParams& p, int mode, int cfg, hipStream_t stream);
+// The same products of modes 1 and 3 on the 256x256 tile in stream-K order
+// over `blocks` blocks (p.partial: sk_max_segments x M x N floats, pitch N,
+// p.partial_stride = M N), then the fixed-order sum of the cut tiles.
+hipError_t gemm_f32_conv_sk(const GemmParams& p, int mode, int blocks, hipStream_t stream);
+int64_t sk_max_segments(int64_t tiles, int64_t ks, int64_t blocks);
 bool gemm_conv_cfg(int cfg);
 // bf16 operands (fp32 accumulation, bias and output). vec: 16-byte loads
 // (8 elements) and 16-byte stores; else 2-byte loads and 4-byte stores.

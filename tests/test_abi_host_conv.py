@@ -78,7 +78,8 @@ def test_conv_gather_needs_no_unfolded_input():
     """Channels-last x and w with C a multiple of 32: the forward product and
     the weight gradient gather the image in their loads, so the forward needs
     no workspace and a backward without dx none for the unfolded input. Other
-    layouts (or the gather switched off) keep the unfolded workspace."""
+    layouts (or the gather switched off) keep the unfolded workspace (plus
+    any split partials after it)."""
     X = cl([2, 32, 9, 9], 0x1000000)
     Wt = cl([16, 32, 3, 3], 0x2000000)
     B = D([16], ptr=0x3000000)
@@ -100,9 +101,9 @@ def test_conv_gather_needs_no_unfolded_input():
     try:
         assert fwd_ws(X, Wt) == 0
         assert fwd(X, Wt, B, Y, st=(0, 1)) == 9        # still validated first
-        assert fwd_ws(X, D([16, 32, 3, 3], ptr=0x2000000)) == col   # [CO][C][KH][KW] weights
-        assert fwd_ws(D([2, 32, 9, 9], ptr=0x1000000), Wt) == col   # [N][C][H][W] input
-        assert fwd_ws(cl([2, 32, 9, 9], 0x1000004), Wt) == col      # x not 16-byte aligned
+        assert fwd_ws(X, D([16, 32, 3, 3], ptr=0x2000000)) >= col   # [CO][C][KH][KW] weights
+        assert fwd_ws(D([2, 32, 9, 9], ptr=0x1000000), Wt) >= col   # [N][C][H][W] input
+        assert fwd_ws(cl([2, 32, 9, 9], 0x1000004), Wt) >= col      # x not 16-byte aligned
         assert bwd_ws(None, dW, None) < col                          # dW gathers: partials only
         assert bwd_ws(dX, dW, None) >= col                           # dU for dx (CO % 32 != 0)
         # CO a multiple of 32 and stride 1: dx gathers dy as well, no dU
@@ -116,7 +117,7 @@ def test_conv_gather_needs_no_unfolded_input():
                                              ctypes.byref(n)) == 0
         assert n.value >= (2 * 5 * 5 * 288 * 4 + 255) // 256 * 256  # stride 2: dU and the fold
         assert b.lib.mt_debug_set(b"conv_gather", 0) == 0
-        assert fwd_ws(X, Wt) == col
+        assert fwd_ws(X, Wt) >= col
         assert bwd_ws(None, dW, None) >= col
     finally:
         b.lib.mt_debug_set(b"conv_gather", 1)

@@ -306,3 +306,60 @@ def test_conv2d_gathered_backward_needs_no_unfolded_workspace():
     b.conv2d_bwd(xd, wd, dyd, dx, dw, db, st, pd)
     torch.cuda.synchronize()
     check(case, x, w, bias, dy, y, dx, dw, db)
+
+
+SK_CASES = [
+    (5, 32, 20, 20, 40, 3, 3, (1, 1), (1, 1), "cl", "cl"),
+    (4, 64, 20, 20, 64, 3, 3, (1, 1), (1, 1), "cl", "cl"),
+    (2, 32, 12, 12, 288, 3, 3, (1, 1), (1, 1), "cl", "cl"),
+    (3, 36, 17, 19, 96, 3, 3, (1, 1), (1, 1), "cl", "cl"),
+]
+
+
+@pytest.mark.parametrize("blocks", [7, 13, 64])
+@pytest.mark.parametrize("case", SK_CASES, ids=[f"s{i}" for i in range(len(SK_CASES))])
+def test_conv2d_stream_k(case, blocks):
+    """The gathered forward and input-gradient products in stream-K order over
+    a forced number of blocks (tiles cut into 1-3 segments at arbitrary
+    stages, several tile rows and columns): against the oracle, and
+    bit-identical on a rerun (segments are summed in a fixed order)."""
+    x, w, bias, dy = make(case, seed=53)
+    try:
+        b.debug_set("cfg", 6)
+        b.debug_set("stream_k", 2)
+        b.debug_set("sk_blocks", blocks)
+        got = run(case, x, w, bias, dy)
+        again = run(case, x, w, bias, dy)
+    finally:
+        b.debug_set("sk_blocks", 0)
+        b.debug_set("stream_k", 1)
+        b.debug_set("cfg", -1)
+    check(case, x, w, bias, dy, *got)
+    for a, c in zip(got, again):
+        assert torch.equal(a, c), "stream-K reruns must be bit-identical"
+
+
+def test_conv2d_stream_k_accumulates_and_needs_its_workspace():
+    """Stream-K with MT_ACCUMULATE (the finish adds C for cut tiles, the
+    product for whole ones); with no workspace the product runs one tile per
+    block and gives the same values up to rounding."""
+    case = SK_CASES[1]
+    x, w, bias, dy = make(case, seed=59)
+    N, C, H, W, CO, KH, KW = case[:7]
+    prior = (torch.randn(N, C, H, W, device=DEV), torch.randn(CO, C, KH, KW, device=DEV),
+             torch.randn(CO, device=DEV))
+    try:
+        b.debug_set("stream_k", 2)
+        b.debug_set("sk_blocks", 13)
+        y, dx, dw, db = run(case, x, w, bias, dy, accumulate=True, prior=prior)
+        check(case, x, w, bias, dy, y, dx, dw, db, prior=prior)
+        st, pd = case[7], case[8]
+        xd, wd, bd = to_dev(x, "cl"), to_dev(w, "cl"), bias.to(DEV)
+        assert b.conv2d_fwd_workspace(xd, wd, bd, y, st, pd) > 0
+        y2 = torch.empty_like(y)
+        b.conv2d_fwd(xd, wd, bd, y2, st, pd)        # no workspace: plain schedule
+        torch.cuda.synchronize()
+        check(case, x, w, bias, dy, y2, None, None, None)
+    finally:
+        b.debug_set("sk_blocks", 0)
+        b.debug_set("stream_k", 1)
