@@ -278,7 +278,8 @@ struct ConvGatherA {
 // contraction (tile rows, BK per stage) and the unfolded columns k as tile
 // columns. A lane's chunk keeps its column, so its tap (u, v) and channel are
 // decoded once per block (C % 4 == 0 keeps a chunk inside one tap); per
-// stage its row's pixel is decoded (two divisions by multiplication).
+// stage its row's pixel is decoded (two divisions by multiplication, on the
+// scalar unit where a load covers one row).
 template <int BN, int BK, int NW>
 struct ConvGatherB {
   using T = DmaTile<4, false, BN, BK>;
@@ -299,7 +300,10 @@ struct ConvGatherB {
       const int r = byte / T::RB;
       const int c = (((byte % T::RB) / 16) ^ T::swz(r)) * 4;
       const int64_t col = n0 + c;
-      rr[j] = (uint32_t)r;
+      // rows of 1 KB or more: one row per instruction, the same in every
+      // lane, so the pixel decode below runs on the scalar unit
+      rr[j] = T::RB >= IB ? (uint32_t)__builtin_amdgcn_readfirstlane(IB * (wave + NW * j) / T::RB)
+                          : (uint32_t)r;
       if (col < N) {
         const uint32_t tap = (uint32_t)col / (uint32_t)g.C;
         const uint32_t u = tap / (uint32_t)g.KW;
