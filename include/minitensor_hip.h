@@ -308,6 +308,29 @@ mt_status mt_reduce_broadcast_grad(const mt_tensor* grad_out, const mt_tensor* g
 mt_status mt_reduce_broadcast_grad_workspace(const mt_tensor* grad_out, const mt_tensor* grad_in,
                                              size_t* bytes);
 
+/* ------------------------------------------------------- workspace query
+ * mt_workspace_bytes: the workspace size of one call, by operation, with the
+ * same tensors the call takes (NULL where the call allows it), for callers
+ * that size workspaces generically. It equals the matching *_workspace
+ * entry point's answer. args, in order:
+ *   MT_OP_MATMUL, MT_OP_MATMUL_REDUCE_INTO   {a, b, c}         (flags 0 / MT_REDUCE_INTO)
+ *   MT_OP_LINEAR_FWD                         {x, w, b, y}      (always 0)
+ *   MT_OP_LINEAR_BWD                         {x, w, dy, dx, dw, db}
+ *   MT_OP_REDUCE_BROADCAST_GRAD              {grad_out, grad_in}
+ *   MT_OP_MSE_LOSS                           {pred, target}
+ * The nonlinearity pullback and the convolution take non-tensor arguments:
+ * use mt_act_bwd_workspace / mt_conv2d_*_workspace. Returns SIZE_MAX for an
+ * unknown op, a wrong count or invalid tensors (message in mt_last_error()).
+ * Host-only.
+ */
+#define MT_OP_MATMUL 0
+#define MT_OP_MATMUL_REDUCE_INTO 1
+#define MT_OP_LINEAR_FWD 2
+#define MT_OP_LINEAR_BWD 3
+#define MT_OP_REDUCE_BROADCAST_GRAD 4
+#define MT_OP_MSE_LOSS 5
+size_t mt_workspace_bytes(int32_t op, const mt_tensor* const* args, int32_t nargs);
+
 /* ------------------------------------------------- host-only shape helpers
  * No GPU needed; results are exact. Shapes are arrays of int64 sizes.
  * mt_broadcast_shape: the broadcast of two shapes (Sec. 3.1).

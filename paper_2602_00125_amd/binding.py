@@ -32,7 +32,8 @@ EXPORTS = ["mt_linear_fwd", "mt_linear_bwd", "mt_linear_bwd_workspace", "mt_matm
            "mt_matmul_shape", "mt_debug_set", "mt_status_str", "mt_last_error",
            "mt_linear_act_fwd", "mt_act_bwd", "mt_act_bwd_workspace", "mt_mse_loss",
            "mt_mse_loss_workspace", "mt_sgd_step", "mt_adam_step", "mt_rmsprop_step",
-           "mt_conv2d_fwd", "mt_conv2d_fwd_workspace", "mt_conv2d_bwd", "mt_conv2d_bwd_workspace"]
+           "mt_conv2d_fwd", "mt_conv2d_fwd_workspace", "mt_conv2d_bwd", "mt_conv2d_bwd_workspace",
+           "mt_workspace_bytes"]
 ACT = {"none": 0, "relu": 1, "sigmoid": 2, "tanh": 3, "gelu": 4}
 
 
@@ -69,14 +70,18 @@ lib.mt_conv2d_fwd_workspace.argtypes = [_P, _P, _P, _P, _i32, _i32, _i32, _i32, 
 lib.mt_conv2d_bwd.argtypes = [_P, _P, _P, _P, _P, _P, _i32, _i32, _i32, _i32, _u32, _vp, _sz, _vp]
 lib.mt_conv2d_bwd_workspace.argtypes = [_P, _P, _P, _P, _P, _P, _i32, _i32, _i32, _i32,
                                         ctypes.POINTER(_sz)]
+lib.mt_workspace_bytes.argtypes = [ctypes.c_int32, ctypes.POINTER(_P), ctypes.c_int32]
 lib.mt_debug_set.argtypes = [ctypes.c_char_p, ctypes.c_int64]
 lib.mt_status_str.argtypes = [ctypes.c_int]
 lib.mt_status_str.restype = ctypes.c_char_p
 lib.mt_last_error.argtypes = []
 lib.mt_last_error.restype = ctypes.c_char_p
 for _name in EXPORTS:
-    if _name not in ("mt_status_str", "mt_last_error"):
+    if _name not in ("mt_status_str", "mt_last_error", "mt_workspace_bytes"):
         getattr(lib, _name).restype = ctypes.c_int
+lib.mt_workspace_bytes.restype = _sz
+OP = {"matmul": 0, "matmul_reduce_into": 1, "linear_fwd": 2, "linear_bwd": 3,
+      "reduce_broadcast_grad": 4, "mse_loss": 5}
 
 
 class MtError(RuntimeError):
@@ -178,6 +183,17 @@ def matmul(a, b, c, accumulate=False, reduce_into=False, workspace=None, stream=
     ptr, nbytes = _ws(workspace)
     _check(lib.mt_matmul(_ref(da), _ref(db_), _ref(dc), flags, ptr, nbytes, _stream(stream)),
            "mt_matmul")
+
+
+def workspace_bytes(op: str, *tensors) -> int:
+    """mt_workspace_bytes: the workspace of operation `op` (a key of OP) for
+    these tensors (None where the call allows it)."""
+    ds = [desc(t) for t in tensors]
+    arr = (_P * max(1, len(ds)))(*[ctypes.pointer(d) if d is not None else _P() for d in ds])
+    n = lib.mt_workspace_bytes(OP[op], arr, len(ds))
+    if n == ctypes.c_size_t(-1).value:
+        raise MtError(9, "mt_workspace_bytes")
+    return int(n)
 
 
 def reduce_broadcast_grad_workspace(grad_out, grad_in) -> int:

@@ -1379,6 +1379,43 @@ mt_status mt_reduce_broadcast_grad_workspace(const mt_tensor* grad_out, const mt
 }
 
 
+size_t mt_workspace_bytes(int32_t op, const mt_tensor* const* args, int32_t nargs) {
+  try {
+    static const int32_t want[] = {3, 3, 4, 6, 2, 2};
+    if (op < 0 || op > MT_OP_MSE_LOSS) {
+      fail(MT_ERR_INVALID, "mt_workspace_bytes: unknown op");
+      return SIZE_MAX;
+    }
+    if (!args || nargs != want[op]) {
+      fail(MT_ERR_INVALID, "mt_workspace_bytes: wrong argument count for this op");
+      return SIZE_MAX;
+    }
+    size_t n = 0;
+    mt_status s = MT_OK;
+    switch (op) {
+      case MT_OP_MATMUL: s = matmul_impl(args[0], args[1], args[2], 0, nullptr, 0, nullptr, &n); break;
+      case MT_OP_MATMUL_REDUCE_INTO:
+        s = matmul_impl(args[0], args[1], args[2], MT_REDUCE_INTO, nullptr, 0, nullptr, &n);
+        break;
+      case MT_OP_LINEAR_FWD:
+        if (!args[0] || !args[1] || !args[3]) s = fail(MT_ERR_NULL, "x, w and y are required");
+        break;
+      case MT_OP_LINEAR_BWD:
+        s = linear_bwd_impl(args[0], args[1], args[2], args[3], args[4], args[5], 0, nullptr, 0,
+                            nullptr, &n);
+        break;
+      case MT_OP_REDUCE_BROADCAST_GRAD:
+        s = reduce_impl(args[0], args[1], 0, nullptr, 0, nullptr, &n);
+        break;
+      case MT_OP_MSE_LOSS: s = mse_impl(args[0], args[1], nullptr, nullptr, nullptr, 0, nullptr, &n); break;
+    }
+    return s == MT_OK ? n : SIZE_MAX;
+  } catch (...) {
+    fail(MT_ERR_INVALID, "internal error");
+    return SIZE_MAX;
+  }
+}
+
 mt_status mt_conv2d_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* b,
                         const mt_tensor* y, int32_t stride_h, int32_t stride_w, int32_t pad_h,
                         int32_t pad_w, void* ws, size_t ws_bytes, void* stream) {

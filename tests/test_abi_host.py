@@ -199,3 +199,36 @@ def test_debug_knobs_validate():
 def test_status_strings():
     for code in range(10):
         assert b.status_str(code)
+
+
+def test_generic_workspace_query_matches_the_per_op_ones():
+    """mt_workspace_bytes gives the per-op *_workspace answer for each op it
+    covers, and SIZE_MAX for an unknown op, a wrong count or bad tensors."""
+    SIZE_MAX = ctypes.c_size_t(-1).value
+
+    def ws(op, *ts):
+        arr = (b._P * len(ts))(*[ctypes.pointer(t) if t is not None else b._P() for t in ts])
+        return b.lib.mt_workspace_bytes(op, arr, len(ts))
+
+    n = ctypes.c_size_t(0)
+    X, W, dY = D([4096, 1024], ptr=0x100000), D([1024, 1024], ptr=0x20000000), D([4096, 1024], ptr=0x30000000)
+    dX, dW, dB = D([4096, 1024], ptr=0x40000000), D([1024, 1024], ptr=0x50000000), D([1024], ptr=0x60000000)
+    assert b.lib.mt_linear_bwd_workspace(R(X), R(W), R(dY), R(dX), R(dW), R(dB), ctypes.byref(n)) == 0
+    assert n.value > 0 and ws(b.OP["linear_bwd"], X, W, dY, dX, dW, dB) == n.value
+    assert ws(b.OP["linear_bwd"], X, W, dY, None, dW, None) >= 0
+    assert ws(b.OP["linear_fwd"], X, W, dB, dY) == 0
+    A = D([16, 1, 509, 257], ptr=0x100000)
+    B = D([1, 8, 257, 383], ptr=0x10000000)
+    C = D([16, 8, 509, 383], ptr=0x20000000)
+    assert b.lib.mt_matmul_workspace(R(A), R(B), R(C), 0, ctypes.byref(n)) == 0
+    assert ws(b.OP["matmul"], A, B, C) == n.value
+    G, Gi = D([16, 8, 509, 257], ptr=0x100000), D([16, 1, 509, 257], ptr=0x900000000)
+    assert b.lib.mt_reduce_broadcast_grad_workspace(R(G), R(Gi), ctypes.byref(n)) == 0
+    assert ws(b.OP["reduce_broadcast_grad"], G, Gi) == n.value
+    P, T = D([1024, 1024], ptr=0x100000), D([1024, 1024], ptr=0x10000000)
+    assert b.lib.mt_mse_loss_workspace(R(P), R(T), ctypes.byref(n)) == 0
+    assert ws(b.OP["mse_loss"], P, T) == n.value
+    assert ws(99, P, T) == SIZE_MAX
+    assert ws(b.OP["mse_loss"], P) == SIZE_MAX                      # wrong count
+    assert ws(b.OP["matmul"], A, D([1, 8, 256, 383], ptr=0x10000000), C) == SIZE_MAX  # shape
+    assert b.lib.mt_last_error()                                    # the reason is recorded
