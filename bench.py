@@ -59,6 +59,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="linear_8192x8192x8192_f32")
+    ap.add_argument("--graph", action="store_true",
+                    help="linear workloads: replay the step from a captured HIP graph (one launch "
+                         "per step instead of one per kernel; for launch-bound sizes)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target wall time of the CPU-oracle baseline sample (0 disables it)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -460,7 +463,22 @@ def main():
         if ev is not None:
             ev[4].record()
 
-    total_ms_step, _ = timed_steps(step, 1, args.steps, args.warmup)
+    run = step
+    if args.graph:
+        # capture one step (its kernels, on the capture stream) and replay it
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+
+        def run(ev=None):
+            graph.replay()
+    total_ms_step, _ = timed_steps(run, 1, args.steps, args.warmup)
     _, per_list = timed_steps(step_per_kernel, 5, args.steps, 1)
     per = dict(zip(["fwd_nt_gemm", "dx_nn_gemm", "dw_tn_gemm", "db_colsum"], per_list))
     total_ms = total_ms_step * args.steps
@@ -501,6 +519,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "M": M, "N": N, "K": K,
                    "inputs": "seeded synthetic, resident in HBM before timing",
+                   "hip_graph": bool(args.graph),
                    "pct_of_mfma_peak": round(100.0 * value / peak, 2)},
         "roofline": {"bound": "mfma", "kernel": dominant, "achieved": round(achieved, 3),
                      "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
