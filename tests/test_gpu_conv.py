@@ -363,3 +363,31 @@ def test_conv2d_stream_k_accumulates_and_needs_its_workspace():
     finally:
         b.debug_set("sk_blocks", 0)
         b.debug_set("stream_k", 1)
+
+
+# Edge cases of the gathered path: one pixel, a window larger than the image
+# (all taps but a few in the padding), a 1-row image, asymmetric strides and
+# paddings, a batch whose pixels do not fill one 128-row tile.
+GATHER_EDGES = [
+    (1, 32, 1, 1, 32, 1, 1, (1, 1), (0, 0), "cl", "cl"),
+    (2, 32, 3, 3, 32, 5, 5, (1, 1), (2, 2), "cl", "cl"),
+    (3, 64, 1, 9, 32, 1, 3, (1, 1), (0, 1), "cl", "cl"),
+    (1, 64, 7, 5, 36, 3, 3, (2, 1), (0, 1), "cl", "cl"),
+    (2, 32, 4, 4, 32, 3, 3, (3, 3), (1, 1), "cl", "cl"),
+    (1, 96, 2, 3, 64, 2, 2, (1, 1), (1, 1), "cl", "cl"),
+]
+
+
+@pytest.mark.parametrize("case", GATHER_EDGES, ids=[f"e{i}" for i in range(len(GATHER_EDGES))])
+def test_conv2d_gather_edges(case):
+    x, w, bias, dy = make(case, seed=67)
+    got = run(case, x, w, bias, dy)
+    check(case, x, w, bias, dy, *got)
+    try:
+        b.debug_set("stream_k", 2)
+        b.debug_set("sk_blocks", 3)
+        got = run(case, x, w, bias, dy)
+    finally:
+        b.debug_set("sk_blocks", 0)
+        b.debug_set("stream_k", 1)
+    check(case, x, w, bias, dy, *got)
