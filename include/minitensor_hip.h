@@ -239,8 +239,10 @@ mt_status mt_rmsprop_step(int32_t n, const mt_tensor* params, const mt_tensor* g
  * those are optional: a shorter workspace runs one tile per block. Sizes
  * from the *_workspace calls. The backward's dx is one product
  * gathering dy where the convolution has stride 1, CO is a multiple of 32 and
- * dx is channels-last (16-byte aligned); otherwise it goes through dU = dY Wf
- * in the workspace and a fold. fp32 only.
+ * dx is channels-last (16-byte aligned); with strides up to the window size
+ * (KH >= sh, KW >= sw) it is one such product per sub-pixel phase of the
+ * stride; otherwise it goes through dU = dY Wf in the workspace and a fold.
+ * fp32 only.
  */
 mt_status mt_conv2d_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* b,
                         const mt_tensor* y, int32_t stride_h, int32_t stride_w, int32_t pad_h,

@@ -913,17 +913,13 @@ bool conv_gather(const ConvPlan& cp, const mt_tensor* x, int mode, mt::ConvGathe
   return true;
 }
 
-// Whether the input gradient of a stride-1 convolution may run as one product
-// gathering dY (dx = V W with V[(n, h, w)][(u, v, co)] = dY[n][h + ph - u][w + pw - v][co]
-// and W read tap by tap) instead of dU = dY Wf and the fold: channels-last
-// dy, w and dx, CO a multiple of 32, 16-byte aligned rows. The description
-// reuses the forward's fields with the roles turned round: the gathered image
-// is dy (CO channels, HO x WO), rows decode over H x W, and the window origin
-// is h + ph (taps enter with a minus sign).
-bool conv_dgrad_gather(const ConvPlan& cp, const mt_tensor* dy, const mt_tensor* w,
-                       const mt_tensor* dx, mt::ConvGather* cg) {
+// Whether the input gradient may be computed by products gathering dy
+// (channels-last dy, w and dx, CO a multiple of 32, 16-byte aligned rows,
+// sizes within the gather's 32-bit offsets).
+bool dgrad_gather_layout_ok(const ConvPlan& cp, const mt_tensor* dy, const mt_tensor* w,
+                            const mt_tensor* dx) {
   const mt::ConvGeom& g = cp.g;
-  if (!g_conv_gather || g_force_vec1 || !g.korder_uvc || g.sh != 1 || g.sw != 1) return false;
+  if (!g_conv_gather || g_force_vec1 || !g.korder_uvc) return false;
   if (g.CO % 32 != 0 || g.C % 4 != 0 || !channels_last(dx) || !aligned16(dx->data)) return false;
   if (!aligned16(dy->data) || !aligned16(w->data) || cp.wpitch % 4 != 0) return false;
   const int64_t lim = (int64_t)1 << 14;
@@ -932,21 +928,69 @@ bool conv_dgrad_gather(const ConvPlan& cp, const mt_tensor* dy, const mt_tensor*
     return false;
   const int64_t ys0 = dy->stride[0], ys2 = dy->stride[2], ys3 = dy->stride[3];
   if (ys0 % 4 || ys2 % 4 || ys3 % 4) return false;
-  const int64_t ext = (int64_t)(g.N - 1) * ys0 + (int64_t)(g.HO - 1) * ys2 +
-                      (int64_t)(g.WO - 1) * ys3 + g.CO;
   if ((int64_t)g.N * ys0 + (int64_t)(g.H + g.ph + 1) * ys2 + (int64_t)(g.W + g.pw + 1) * ys3 +
           g.CO >= ((int64_t)1 << 29))
     return false;
-  if ((int64_t)g.N * g.H * g.W >= ((int64_t)1 << 31) - 64) return false;
+  return (int64_t)g.N * g.H * g.W < ((int64_t)1 << 31) - 64;
+}
+
+// The gathered description of dy for the input-gradient products, with the
+// roles of the forward's fields turned round: the gathered image is dy (CO
+// channels, HO x WO), the rows decode over rows x cols pixels per image and
+// the window origin of row (i, j) is (i - ph', j - pw'), taps entering with a
+// minus sign. For a stride-1 convolution rows x cols = H x W and ph' = -ph.
+void dgrad_cg(const ConvPlan& cp, const mt_tensor* dy, int64_t rows, int64_t cols, int64_t ph_,
+              int64_t pw_, int64_t taps_w, mt::ConvGather* cg) {
+  const mt::ConvGeom& g = cp.g;
+  const int64_t ys0 = dy->stride[0], ys2 = dy->stride[2], ys3 = dy->stride[3];
   std::memset(cg, 0, sizeof(*cg));
   cg->x = (const float*)dy->data;
-  cg->x_bytes = (uint32_t)(ext * 4);
-  cg->C = g.CO; cg->H = g.HO; cg->W = g.WO; cg->KW = g.KW;
-  cg->sh = 1; cg->sw = 1; cg->ph = -g.ph; cg->pw = -g.pw;
-  cg->HO = g.H; cg->WO = g.W;
+  cg->x_bytes = (uint32_t)(((int64_t)(g.N - 1) * ys0 + (int64_t)(g.HO - 1) * ys2 +
+                            (int64_t)(g.WO - 1) * ys3 + g.CO) * 4);
+  cg->C = g.CO; cg->H = g.HO; cg->W = g.WO; cg->KW = (int32_t)taps_w;
+  cg->sh = 1; cg->sw = 1; cg->ph = (int32_t)ph_; cg->pw = (int32_t)pw_;
+  cg->HO = (int32_t)rows; cg->WO = (int32_t)cols;
   cg->xs0 = (int32_t)ys0; cg->xs2 = (int32_t)ys2; cg->xs3 = (int32_t)ys3;
-  fast_div_params(g.W, &cg->wo_mag, &cg->wo_shift);
-  fast_div_params(g.H, &cg->ho_mag, &cg->ho_shift);
+  fast_div_params(cols, &cg->wo_mag, &cg->wo_shift);
+  fast_div_params(rows, &cg->ho_mag, &cg->ho_shift);
+}
+
+// Whether the input gradient of a stride-1 convolution may run as one product
+// gathering dy (dx = V W with V[(n, h, w)][(u, v, co)] = dY[n][h + ph - u][w + pw - v][co]
+// and W read tap by tap) instead of dU = dY Wf and the fold.
+bool conv_dgrad_gather(const ConvPlan& cp, const mt_tensor* dy, const mt_tensor* w,
+                       const mt_tensor* dx, mt::ConvGather* cg) {
+  const mt::ConvGeom& g = cp.g;
+  if (g.sh != 1 || g.sw != 1 || !dgrad_gather_layout_ok(cp, dy, w, dx)) return false;
+  dgrad_cg(cp, dy, g.H, g.W, -g.ph, -g.pw, g.KW, cg);
+  return true;
+}
+
+// One sub-pixel phase (a, b) of a strided input gradient: the dx pixels with
+// (h + ph) % sh == a and (w + pw) % sw == b, i.e. h = a - ph + sh i'. Only the
+// taps u = a + sh t, v = b + sw r reach them, from dY row i' - t, column
+// j' - r: a stride-1 gathered product over those taps. Returns false when the
+// phase holds no pixel.
+struct DgradPhase {
+  mt::ConvGather cg;
+  int64_t M, K;
+};
+bool dgrad_phase(const ConvPlan& cp, const mt_tensor* dy, int a, int b, DgradPhase* ph) {
+  const mt::ConvGeom& g = cp.g;
+  auto first = [](int64_t pad, int64_t r, int64_t s) { return pad > r ? (pad - r + s - 1) / s : 0; };
+  const int64_t i0 = first(g.ph, a, g.sh), j0 = first(g.pw, b, g.sw);
+  // pixels: a - ph + sh i' < H
+  const int64_t i_end = (g.H - a + g.ph + g.sh - 1) / g.sh, j_end = (g.W - b + g.pw + g.sw - 1) / g.sw;
+  const int64_t rows = i_end - i0, cols = j_end - j0;
+  if (rows <= 0 || cols <= 0) return false;
+  const int64_t th = (g.KH - a + g.sh - 1) / g.sh, tw = (g.KW - b + g.sw - 1) / g.sw;
+  dgrad_cg(cp, dy, rows, cols, -i0, -j0, tw, &ph->cg);
+  ph->cg.u0 = a; ph->cg.v0 = b; ph->cg.su = g.sh; ph->cg.sv = g.sw; ph->cg.wKW = g.KW;
+  ph->cg.eH = g.H; ph->cg.eW = g.W; ph->cg.esh = g.sh; ph->cg.esw = g.sw;
+  ph->cg.h0 = (int32_t)(a - g.ph + g.sh * i0);
+  ph->cg.w0 = (int32_t)(b - g.pw + g.sw * j0);
+  ph->M = (int64_t)g.N * rows * cols;
+  ph->K = th * tw * g.CO;
   return true;
 }
 
@@ -1105,6 +1149,10 @@ mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
   // mirrored taps), its rows the input pixels
   GemmCall gdxg{};
   const bool dx_gather = dx && conv_dgrad_gather(cp, dy, w, dx, &gdxg.p.cg);
+  // strided: one gathered product per sub-pixel phase, where every phase has
+  // taps (KH >= sh, KW >= sw)
+  const bool dx_phased = dx && !dx_gather && (g.sh > 1 || g.sw > 1) && g.KH >= g.sh &&
+                         g.KW >= g.sw && dgrad_gather_layout_ok(cp, dy, w, dx);
   size_t need_dx = 0;
   if (dx_gather) {
     const mt::ConvGather dcg = gdxg.p.cg;
@@ -1132,7 +1180,7 @@ mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
   // the unfolded matrix (U for an unfolded dW, then dU for an unfolded dx)
   // heads the workspace; split or stream-K partials follow (the products run
   // one after another and share them)
-  const size_t col_need = ((dx && !dx_gather) || (dw && !gdw.conv)) ? cp.col_bytes : 0;
+  const size_t col_need = ((dx && !dx_gather && !dx_phased) || (dw && !gdw.conv)) ? cp.col_bytes : 0;
   const size_t need = col_need + std::max(std::max(need_dw, need_db), need_dx);
   if (ws_query) {
     *ws_query = need;
@@ -1168,6 +1216,33 @@ mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
   }
   if (dx && dx_gather && cp.M > 0) {
     if ((s = launch_gemm(gdxg, stream, rest_bytes ? rest : nullptr, rest_bytes))) return s;
+  } else if (dx && dx_phased && cp.M > 0) {
+    for (int a = 0; a < g.sh; ++a)
+      for (int bb = 0; bb < g.sw; ++bb) {
+        DgradPhase ph;
+        if (!dgrad_phase(cp, dy, a, bb, &ph)) continue;
+        GemmCall gp{};
+        init_params(&gp.p);
+        gp.p.cg = ph.cg;
+        gp.p.a = dy->data;
+        gp.p.b = w->data;
+        gp.p.c = (float*)dx->data;
+        gp.p.M = ph.M;
+        gp.p.N = g.C;
+        gp.p.K = ph.K;
+        gp.p.lda = 0;
+        gp.p.ldb = cp.wpitch;
+        gp.p.ldc = g.C;
+        gp.p.accumulate = acc;
+        gp.a_kc = true;
+        gp.b_kc = false;
+        gp.bf16 = false;
+        gp.vec = true;
+        gp.cfg = -1;
+        gp.conv = 4;
+        // no split: the phase's rows land directly in dx
+        if ((s = launch_gemm(gp, stream, nullptr, 0))) return s;
+      }
   } else if (dx && cp.M > 0) {
     // dU = dY Wf into the workspace (U is no longer needed), then the fold
     GemmCall gdx{};

@@ -465,13 +465,14 @@ void gemm_dma_kernel(const GemmParams p) {
 // The convolution products with an operand gathered by the loads: CONV_ 1 the
 // forward (y = U Wf^T + b, NT), 2 the weight gradient (dW = dY^T U, TN), 3
 // the input gradient of a stride-1 convolution (dx = V W, NN, V gathered from
-// dY: V[(n, h, w)][(u, v, co)] = dY[n][h + ph - u][w + pw - v][co]).
+// dY: V[(n, h, w)][(u, v, co)] = dY[n][h + ph - u][w + pw - v][co]), 4 one
+// sub-pixel phase of a strided convolution's input gradient.
 template <int CONV_, int BM, int BN, int BK, int WGM, int WGN, int NS, bool KTAIL, int WAVES_PER_EU>
 __global__ __launch_bounds__(WGM * WGN * 64)
 __attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
 void conv_dma_kernel(const GemmParams p) {
   using T = float;
-  constexpr bool A_KC = CONV_ != 2, B_KC = CONV_ == 1, EPI = false, VEC_C = true;
+  constexpr bool A_KC = CONV_ != 2, B_KC = CONV_ == 1, EPI = false, VEC_C = true;  // CONV_ 1..4
   constexpr int DMA_G0 = 1, DMA_GS = 1, DMA_LANE = 16, CONV = CONV_;
   constexpr bool SK = false, sk_part = false;
   constexpr int64_t sk_t = 0, sk_ka = 0, sk_kb = 0;

@@ -212,6 +212,7 @@ hipError_t gemm_f32_conv(const GemmParams& p, int mode, int cfg, hipStream_t str
   if (mode == 1) return conv_cfg<1>(p, cfg, stream);
   if (mode == 2) return conv_cfg<2>(p, cfg, stream);
   if (mode == 3) return conv_cfg<3>(p, cfg, stream);
+  if (mode == 4) return conv_cfg<4>(p, cfg, stream);
   return hipErrorInvalidValue;
 }
 

@@ -30,6 +30,12 @@ struct ConvGather {
   int32_t xs0, xs2, xs3;  // element strides of x over n, h, w
   uint32_t wo_mag, ho_mag;
   int32_t wo_shift, ho_shift;
+  // one sub-pixel phase of a strided input gradient (CONV 4): the phase's
+  // taps are (u0 + su t, v0 + sv r) of the weight's KH x wKW; its rows, in
+  // HO x WO order per image, are the dx pixels (h0 + sh i, w0 + sw j) of an
+  // eH x eW image
+  int32_t u0, v0, su, sv, wKW;
+  int32_t eH, eW, h0, w0, esh, esw;
 };
 
 struct GemmParams {

@@ -39,7 +39,8 @@ hipError_t gemm_f32(const GemmParams& p, bool a_kc, bool b_kc, bool vec, int cfg
 // the forward (A = unfolded input, NT; K a multiple of 32), mode 2 the weight
 // gradient (B = unfolded input, TN), mode 3 the input gradient of a stride-1
 // convolution (A = dY unfolded over the mirrored taps, B = the weights tap by
-// tap, NN; K a multiple of 32). fp32, 16-byte loads and stores, on the
+// tap, NN; K a multiple of 32), mode 4 one sub-pixel phase of a strided
+// convolution's input gradient (no split: its rows go straight to dx). fp32, 16-byte loads and stores, on the
 // DMA tiles 256x256 (cfg 6) and 128x128 (cfg 10, 11) only.
 hipError_t gemm_f32_conv(const GemmParams& p, int mode, int cfg, hipStream_t stream);
 // The same products of modes 1 and 3 on the 256x256 tile in stream-K order

@@ -391,3 +391,39 @@ def test_conv2d_gather_edges(case):
         b.debug_set("sk_blocks", 0)
         b.debug_set("stream_k", 1)
     check(case, x, w, bias, dy, *got)
+
+
+# Strided convolutions whose input gradient runs as one gathered product per
+# sub-pixel phase (CO % 32 == 0, KH >= sh, KW >= sw), and one (1x1 window,
+# stride 2) that keeps dU and the fold.
+PHASE_CASES = [
+    (2, 8, 9, 9, 32, 3, 3, (2, 2), (1, 1), "cl", "cl"),
+    (2, 16, 10, 7, 64, 5, 3, (2, 1), (2, 0), "cl", "cl"),
+    (1, 12, 11, 13, 32, 3, 4, (3, 2), (1, 1), "cl", "cl"),
+    (2, 32, 28, 28, 64, 3, 3, (2, 2), (1, 1), "cl", "cl"),
+    (3, 4, 12, 12, 32, 4, 4, (2, 2), (0, 0), "cl", "cl"),
+    (2, 8, 8, 8, 32, 1, 1, (2, 2), (0, 0), "cl", "cl"),
+]
+
+
+@pytest.mark.parametrize("case", PHASE_CASES, ids=[f"p{i}" for i in range(len(PHASE_CASES))])
+def test_conv2d_strided_input_gradient_by_phases(case):
+    x, w, bias, dy = make(case, seed=71)
+    got = run(case, x, w, bias, dy)
+    check(case, x, w, bias, dy, *got)
+    N, C, H, W, CO, KH, KW = case[:7]
+    prior = (torch.randn(N, C, H, W, device=DEV), torch.randn(CO, C, KH, KW, device=DEV),
+             torch.randn(CO, device=DEV))
+    got = run(case, x, w, bias, dy, outputs=("dx",), accumulate=True, prior=prior)
+    check(case, x, w, bias, dy, got[0], got[1], None, None, prior=prior)
+
+
+def test_conv2d_strided_phases_need_no_unfolded_workspace():
+    case = PHASE_CASES[3]
+    x, w, bias, dy = make(case, seed=73)
+    N, C, H, W, CO, KH, KW, st, pd, wlay, xlay = case
+    xd, wd, dyd = to_dev(x, xlay), to_dev(w, wlay), to_dev(dy, "cl")
+    dx = torch.empty(N, C, H, W, device=DEV).contiguous(memory_format=CL)
+    HO, WO = dy.shape[2:]
+    col = N * HO * WO * C * KH * KW * 4
+    assert b.conv2d_bwd_workspace(xd, wd, dyd, dx, None, None, st, pd) < col
