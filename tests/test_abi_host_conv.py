@@ -115,7 +115,11 @@ def test_conv_gather_needs_no_unfolded_input():
         dY5 = cl([2, 32, 5, 5], 0x4000000)
         assert b.lib.mt_conv2d_bwd_workspace(R(X), R(W32), R(dY5), R(dX), R(dW32), None, 2, 2, 1, 1,
                                              ctypes.byref(n)) == 0
-        assert n.value >= (2 * 5 * 5 * 288 * 4 + 255) // 256 * 256  # stride 2: dU and the fold
+        assert n.value < (2 * 5 * 5 * 288 * 4 + 255) // 256 * 256   # stride 2: sub-pixel phases
+        dY3 = cl([2, 32, 3, 3], 0x4000000)                           # stride 4 > 3x3 window
+        assert b.lib.mt_conv2d_bwd_workspace(R(X), R(W32), R(dY3), R(dX), R(dW32), None, 4, 4, 1, 1,
+                                             ctypes.byref(n)) == 0
+        assert n.value >= (2 * 3 * 3 * 288 * 4 + 255) // 256 * 256  # a phase without taps: dU and the fold
         assert b.lib.mt_debug_set(b"conv_gather", 0) == 0
         assert fwd_ws(X, Wt) >= col
         assert bwd_ws(None, dW, None) >= col
