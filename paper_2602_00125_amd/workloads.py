@@ -193,10 +193,16 @@ CONV2D_32x256x56x56_256x3x3_F32 = ConvWorkload(
     stride=(1, 1), pad=(1, 1),
     dist={"x": N01, "w": _u(1 / math.sqrt(256 * 9)), "b": _u(1 / math.sqrt(256 * 9)), "dy": N01})
 
+# the same layer downsampling (stride 2): its input gradient runs by sub-pixel phases
+CONV2D_32x256x56x56_256x3x3_S2_F32 = ConvWorkload(
+    "conv2d_32x256x56x56_256x3x3_s2p1_f32", N=32, C=256, H=56, W=56, CO=256, KH=3, KW=3,
+    stride=(2, 2), pad=(1, 1),
+    dist={"x": N01, "w": _u(1 / math.sqrt(256 * 9)), "b": _u(1 / math.sqrt(256 * 9)), "dy": N01})
+
 WORKLOADS = {w.name: w for w in (LINEAR_64x32x128_F32, LINEAR_4096x1024x1024_F32,
                                  LINEAR_8192x8192x8192_F32, BMM_BCAST_16x1x509x257_1x8x257x383_F32,
                                  LINEAR_16384x8192x8192_BF16, MLP2_8192x8192x8192x8192_F32_GELU,
-                                 CONV2D_32x256x56x56_256x3x3_F32)}
+                                 CONV2D_32x256x56x56_256x3x3_F32, CONV2D_32x256x56x56_256x3x3_S2_F32)}
 
 
 def linear(M, N, K, dtype="f32", dist=None, seed=0, name=None) -> LinearWorkload:
