@@ -530,5 +530,43 @@ void conv_dma_sk_kernel(const GemmParams p) {
   }
 }
 
+// All sub-pixel phases of a strided input gradient in one grid (phases in
+// the order of the table, longest contraction first, so that the longest
+// tiles start first): the block finds its phase, rewrites the phase's fields
+// of the description and computes one whole tile of it.
+template <int BM, int BN, int BK, int WGM, int WGN, int NS, int WAVES_PER_EU>
+__global__ __launch_bounds__(WGM * WGN * 64)
+__attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
+void conv_dgrad_phases_kernel(const GemmParams p0, const ConvPhases tab) {
+  using T = float;
+  constexpr bool A_KC = true, B_KC = false, EPI = false, VEC_C = true, KTAIL = false;
+  constexpr int DMA_G0 = 1, DMA_GS = 1, DMA_LANE = 16, CONV = 4;
+  constexpr bool SK = true, sk_part = false;
+  constexpr int sk_slot = 0;
+  int k = 0;
+  while (k + 1 < tab.n && (int32_t)blockIdx.x >= tab.tile0[k + 1]) ++k;
+  const ConvPhase& f = tab.ph[k];
+  GemmParams p = p0;
+  p.M = f.M;
+  p.K = f.K;
+  p.tiles_m = f.tiles_m;
+  p.cg.u0 = f.u0;
+  p.cg.v0 = f.v0;
+  p.cg.ph = f.ph;
+  p.cg.pw = f.pw;
+  p.cg.HO = f.rows;
+  p.cg.WO = f.cols;
+  p.cg.KW = f.kw;
+  p.cg.h0 = f.h0;
+  p.cg.w0 = f.w0;
+  p.cg.wo_mag = f.wo_mag;
+  p.cg.ho_mag = f.ho_mag;
+  p.cg.wo_shift = f.wo_shift;
+  p.cg.ho_shift = f.ho_shift;
+  const int64_t sk_t = (int64_t)blockIdx.x - tab.tile0[k];
+  const int64_t sk_ka = 0, sk_kb = (f.K + BK - 1) / BK;
+#include "gemm_dma_body.inc"
+}
+
 }  // namespace gemm
 }  // namespace mt

@@ -194,6 +194,24 @@ hipError_t gemm_f32_conv_sk(const GemmParams& p, int mode, int blocks, hipStream
   return hipGetLastError();
 }
 
+// Every sub-pixel phase of a strided input gradient in one grid on the
+// 256x256 tile (p: the shared description, N = C; tab: the phases, their
+// tile counts summed in tile0).
+hipError_t gemm_f32_conv_phases(const GemmParams& p, const ConvPhases& tab, hipStream_t stream) {
+  if (tab.n <= 0 || tab.n > kMaxConvPhases || p.N % 4 != 0) return hipErrorInvalidValue;
+  for (int k = 0; k < tab.n; ++k)
+    if (tab.ph[k].K % 32 != 0 || tab.ph[k].M <= 0) return hipErrorInvalidValue;
+  GemmParams q = p;
+  q.tiles_n = (int32_t)((p.N + 255) / 256);
+  q.splits = 1;
+  const int64_t blocks = tab.tile0[tab.n];
+  if (blocks <= 0) return hipSuccess;
+  if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL((gemm::conv_dgrad_phases_kernel<256, 256, 32, 2, 4, 2, 2>), dim3((unsigned)blocks),
+                     dim3(512), 0, stream, q, tab);
+  return hipGetLastError();
+}
+
 int64_t sk_max_segments(int64_t tiles, int64_t ks, int64_t blocks) {
   const int64_t U = tiles * ks;
   int64_t most = 1;

@@ -38,6 +38,23 @@ struct ConvGather {
   int32_t eH, eW, h0, w0, esh, esw;
 };
 
+// The sub-pixel phases of one strided input gradient, launched as one grid:
+// phase k owns blocks tile0[k] .. tile0[k+1]-1 (one tile each) and replaces
+// these fields of the launch description (the rest is shared).
+constexpr int kMaxConvPhases = 16;
+struct ConvPhase {
+  int64_t M, K;
+  int32_t tiles_m;
+  int32_t u0, v0, ph, pw, rows, cols, kw, h0, w0;
+  uint32_t wo_mag, ho_mag;
+  int32_t wo_shift, ho_shift;
+};
+struct ConvPhases {
+  int32_t n;
+  int32_t tile0[kMaxConvPhases + 1];
+  ConvPhase ph[kMaxConvPhases];
+};
+
 struct GemmParams {
   const void* a;
   const void* b;

@@ -48,6 +48,9 @@ hipError_t gemm_f32_conv(const GemmParams& p, int mode, int cfg, hipStream_t str
 // p.partial_stride = M N), then the fixed-order sum of the cut tiles.
 hipError_t gemm_f32_conv_sk(const GemmParams& p, int mode, int blocks, hipStream_t stream);
 int64_t sk_max_segments(int64_t tiles, int64_t ks, int64_t blocks);
+// All sub-pixel phases of a strided input gradient (mode 4) in one launch on
+// the 256x256 tile: phase k computes tiles tile0[k] .. tile0[k+1]-1.
+hipError_t gemm_f32_conv_phases(const GemmParams& p, const ConvPhases& tab, hipStream_t stream);
 bool gemm_conv_cfg(int cfg);
 // bf16 operands (fp32 accumulation, bias and output). vec: 16-byte loads
 // (8 elements) and 16-byte stores; else 2-byte loads and 4-byte stores.

@@ -406,16 +406,23 @@ PHASE_CASES = [
 ]
 
 
+@pytest.mark.parametrize("grid", [0, 2])
 @pytest.mark.parametrize("case", PHASE_CASES, ids=[f"p{i}" for i in range(len(PHASE_CASES))])
-def test_conv2d_strided_input_gradient_by_phases(case):
+def test_conv2d_strided_input_gradient_by_phases(case, grid):
+    """A launch per phase (grid 0) or every phase in one grid of 256x256 tiles
+    (grid 2), with and without MT_ACCUMULATE."""
     x, w, bias, dy = make(case, seed=71)
-    got = run(case, x, w, bias, dy)
-    check(case, x, w, bias, dy, *got)
-    N, C, H, W, CO, KH, KW = case[:7]
-    prior = (torch.randn(N, C, H, W, device=DEV), torch.randn(CO, C, KH, KW, device=DEV),
-             torch.randn(CO, device=DEV))
-    got = run(case, x, w, bias, dy, outputs=("dx",), accumulate=True, prior=prior)
-    check(case, x, w, bias, dy, got[0], got[1], None, None, prior=prior)
+    try:
+        b.debug_set("phase_grid", grid)
+        got = run(case, x, w, bias, dy)
+        check(case, x, w, bias, dy, *got)
+        N, C, H, W, CO, KH, KW = case[:7]
+        prior = (torch.randn(N, C, H, W, device=DEV), torch.randn(CO, C, KH, KW, device=DEV),
+                 torch.randn(CO, device=DEV))
+        got = run(case, x, w, bias, dy, outputs=("dx",), accumulate=True, prior=prior)
+        check(case, x, w, bias, dy, got[0], got[1], None, None, prior=prior)
+    finally:
+        b.debug_set("phase_grid", 1)
 
 
 def test_conv2d_strided_phases_need_no_unfolded_workspace():
