@@ -262,14 +262,18 @@ size_t plan_gemm(GemmCall& g, bool may_split) {
   g.sk = 0;
   if (!may_split || p.M == 0 || p.N == 0 || p.keep_count == 0 || stages == 0) return 0;
   // The gathered forward / input-gradient products on the 256x256 tile (one
-  // block per CU) whose tiles leave the last wave under 90% full: stream-K,
-  // every CU taking an equal share of the tile-major K-stages (at least
-  // kDmaMinRunStages each); cut tiles are summed by a finish pass
+  // block per CU) whose tiles leave CUs idle: stream-K, every CU taking an
+  // equal share of the tile-major K-stages; cut tiles are summed by a finish
+  // pass
   if ((g.conv == 1 || g.conv == 3) && g.cfg == mt::kCfgDma256x256 && g_stream_k) {
     const int64_t G = g_sk_blocks > 0 ? g_sk_blocks : 256;
     const int64_t T = cdiv(p.M, 256) * cdiv(p.N, 256);
-    const bool ragged = T > G && (double)T / (double)(cdiv(T, G) * G) < 0.9 &&
-                        T * stages >= G * kDmaMinRunStages;
+    // more tiles than CUs with a last wave under 90% full, or fewer tiles
+    // than CUs (a split by whole runs leaves CUs idle) with at least 16
+    // stages per block
+    const bool ragged = (T > G && (double)T / (double)(cdiv(T, G) * G) < 0.9 &&
+                         T * stages >= G * kDmaMinRunStages) ||
+                        (T < G && T * stages >= G * 16);
     // (at least one stage per block keeps the block boundaries distinct)
     if ((g_stream_k == 2 && T * stages >= G) || ragged) {
       g.sk = (int)G;
