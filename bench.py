@@ -35,10 +35,12 @@ METRIC = "TFLOP/s for linear fwd+bwd (3 GEMMs) at M=N=K=8192 fp32; % MFMA peak"
 KERNEL_SOURCES = {
     "gemm": ["paper_2602_00125_amd/csrc/gemm_kernel.hpp", "paper_2602_00125_amd/csrc/gemm_dma.hpp",
              "paper_2602_00125_amd/csrc/gemm_dma_body.inc", "paper_2602_00125_amd/csrc/gemm_f32.hip",
-             "paper_2602_00125_amd/csrc/gemm_params.hpp", "paper_2602_00125_amd/csrc/capi.cpp"],
+             "paper_2602_00125_amd/csrc/gemm_params.hpp", "paper_2602_00125_amd/csrc/capi.cpp",
+             "paper_2602_00125_amd/csrc/host.hpp"],
     "gemm_bf16": ["paper_2602_00125_amd/csrc/gemm_kernel.hpp", "paper_2602_00125_amd/csrc/gemm_dma.hpp",
                   "paper_2602_00125_amd/csrc/gemm_dma_body.inc", "paper_2602_00125_amd/csrc/gemm_bf16.hip",
-                  "paper_2602_00125_amd/csrc/gemm_params.hpp", "paper_2602_00125_amd/csrc/capi.cpp"],
+                  "paper_2602_00125_amd/csrc/gemm_params.hpp", "paper_2602_00125_amd/csrc/capi.cpp",
+                  "paper_2602_00125_amd/csrc/host.hpp"],
     "colsum": ["paper_2602_00125_amd/csrc/reduce.hip", "paper_2602_00125_amd/csrc/capi.cpp"],
 }
 
