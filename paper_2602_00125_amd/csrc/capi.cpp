@@ -170,6 +170,11 @@ int choose_splits(int64_t blocks, int64_t stages, int cfg) {
     return s < 1 ? 1 : (int)s;
   }
   if (blocks >= 512) return 1;
+  // the 128x128 DMA tiles with a block on every CU already keep the matrix
+  // cores as busy as two blocks per CU do, so a split only adds its finish
+  // (measured on 4096 x 1024 x 1024, dX unsplit: 121 TFLOP/s against 103-105
+  // in two runs)
+  if ((cfg == mt::kCfgDma128x128 || cfg == mt::kCfgDma128x128w8) && blocks >= 256) return 1;
   // two blocks per CU: at most 512 blocks, so that the grid stays one wave
   int64_t s = 512 / blocks;
   s = std::min<int64_t>(s, stages / 8);

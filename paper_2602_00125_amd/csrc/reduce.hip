@@ -127,6 +127,47 @@ __global__ __launch_bounds__(256) void splitk_finish_kernel(const float* partial
   *dst = accumulate ? *dst + s : s;
 }
 
+// The same sums four columns a lane with 16-byte accesses (N, ldc and every
+// base a multiple of 4 floats): blockIdx.x covers 1024 columns, blockIdx.y
+// strides over the rows. Each element is summed in the same order as above.
+__global__ __launch_bounds__(256) void splitk_finish4_kernel(const float* partial, int splits,
+                                                             int64_t M, int64_t N, float* c,
+                                                             int64_t ldc, const float* bias,
+                                                             int accumulate) {
+  const int64_t n = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (n >= N) return;
+  const int64_t MN = M * N;
+  float4 bb = {0.f, 0.f, 0.f, 0.f};
+  if (bias) bb = *(const float4*)(bias + n);
+  for (int64_t m = blockIdx.y; m < M; m += gridDim.y) {
+    const float* src = partial + m * N + n;
+    float4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+    for (int p = 0; p < splits; ++p) {
+      const float4 v = *(const float4*)(src + (int64_t)p * MN);
+      s.x += v.x;
+      s.y += v.y;
+      s.z += v.z;
+      s.w += v.w;
+    }
+    if (bias) {
+      s.x += bb.x;
+      s.y += bb.y;
+      s.z += bb.z;
+      s.w += bb.w;
+    }
+    float4* dst = (float4*)(c + m * ldc + n);
+    if (accumulate) {
+      const float4 d = *dst;
+      s.x = d.x + s.x;
+      s.y = d.y + s.y;
+      s.z = d.z + s.z;
+      s.w = d.w + s.w;
+    }
+    *dst = s;
+  }
+}
+
 __global__ __launch_bounds__(256) void fill_kernel(float* out, int64_t n, float v) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i < n) out[i] = v;
@@ -275,6 +316,13 @@ hipError_t splitk_finish(const float* partial, int splits, int64_t M, int64_t N,
                          int64_t ldc, const float* bias, bool accumulate, hipStream_t stream) {
   const int64_t n = M * N;
   if (n <= 0) return hipSuccess;
+  auto a16 = [](const void* q) { return ((uintptr_t)q & 15) == 0; };
+  if (N % 4 == 0 && ldc % 4 == 0 && a16(partial) && a16(c) && (!bias || a16(bias))) {
+    const int64_t rows = M < 65535 ? M : 65535;
+    hipLaunchKernelGGL(splitk_finish4_kernel, dim3((unsigned)((N / 4 + 255) / 256), (unsigned)rows),
+                       dim3(256), 0, stream, partial, splits, M, N, c, ldc, bias, (int)accumulate);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(splitk_finish_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream,
                      partial, splits, M, N, c, ldc, bias, (int)accumulate);
   return hipGetLastError();
