@@ -59,7 +59,9 @@ def parse():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=-1,
+                    help="untimed warm-up steps (default: as many as take about a second, at "
+                         "least 5, so that the GPU clock has ramped up before timing starts)")
     ap.add_argument("--workload", default="linear_8192x8192x8192_f32")
     ap.add_argument("--graph", action="store_true",
                     help="linear workloads: replay the step from a captured HIP graph (one launch "
@@ -125,13 +127,28 @@ def cpu_baseline(inp, seconds: float):
                       f"products with the |a*b| bound) in {el:.1f} s; TFLOP/s = 2*MACs/s"}
 
 
+WARMUP_USED = [None]  # warm-up steps of the run's timed pass (reported as "warmup")
+
+
 def timed_steps(step, n_events: int, steps: int, warmup: int):
     """Warm up, then time `steps` steps (events between their calls when
-    n_events > 1); returns (mean ms per step, mean ms between events)."""
+    n_events > 1); returns (mean ms per step, mean ms between events).
+    warmup < 0: steps, each waited for, until about a second has passed (at
+    least 5)."""
     import torch
 
-    for _ in range(warmup):
-        step()
+    if warmup < 0:
+        t = time.perf_counter()
+        warmup = 0
+        while warmup < 5 or (time.perf_counter() - t < 1.0 and warmup < 100000):
+            step()
+            torch.cuda.synchronize()
+            warmup += 1
+    else:
+        for _ in range(warmup):
+            step()
+    if WARMUP_USED[0] is None:  # the first call is the timed pass of the run
+        WARMUP_USED[0] = warmup
     torch.cuda.synchronize()
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(n_events)] for _ in range(steps)]
     if n_events < 2:
@@ -188,7 +205,7 @@ def bench_bmm(args, w, inp, dev):
     achieved = (w.flops() / 3) / (per[dominant] * 1e-3) / 1e12
     out = {"metric": f"TFLOP/s for broadcast matmul fwd+bwd (3 products) on {args.workload}",
            "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
-           "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+           "warmup": WARMUP_USED[0], "ms_per_step": round(ms, 4), "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
            "config": {"workload": args.workload, "a": list(w.ashape), "b": list(w.bshape),
                       "pct_of_mfma_peak": round(100.0 * value / FP32_MFMA_PEAK_TFLOPS, 2)},
@@ -305,7 +322,7 @@ def bench_mlp(args, w, inp, dev):
     out = {"metric": f"TFLOP/s for a two-layer perceptron training step (5 GEMMs + GELU, MSE, "
                      f"Adam) on {args.workload}",
            "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
-           "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+           "warmup": WARMUP_USED[0], "ms_per_step": round(ms_step, 4), "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
            "config": {"workload": args.workload, "M": M, "D0": w.D0, "D1": D1, "D2": D2,
                       "act": w.act, "optimizer": "adam",
@@ -395,7 +412,7 @@ def bench_conv(args, w, inp, dev):
     value = w.flops() / (ms * 1e-3) / 1e12
     out = {"metric": f"TFLOP/s for a 2-D convolution fwd+bwd (3 products) on {args.workload}",
            "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
-           "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+           "warmup": WARMUP_USED[0], "ms_per_step": round(ms, 4), "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
            "config": {"workload": args.workload, "x": [w.N, w.C, w.H, w.W],
                       "w": [w.CO, w.C, w.KH, w.KW], "stride": list(st), "pad": list(pd),
@@ -512,7 +529,7 @@ def main():
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": args.warmup,
+        "warmup": WARMUP_USED[0],
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "weak",

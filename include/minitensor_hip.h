@@ -350,9 +350,10 @@ mt_status mt_matmul_shape(int32_t na, const int64_t* a, int32_t nb, const int64_
  * 1 = 256x128, 2 = 128x256, 3 = 128x128, 4 = 64x64, 5 = 256x256 with 8 waves;
  * tiles streamed straight into an LDS ring 6 = 256x256 with 8 waves,
  * 7 = 256x256 with 4 waves, 8 = 256x128, 9 = 128x256, 10 = 128x128,
- * 11 = 128x128 with 8 waves; fp32 operands that do not allow 16-byte loads run
- * on tiles 6, 8, 9, 10 with 4-byte lanes (11 maps to 10), else at 128x128 or
- * 64x64; bf16 ones at 128x128 or 64x64); "vec1"
+ * 11 = 128x128 with 8 waves, 12 = 128x128 with 8 waves and 64-deep fp32
+ * K-stages (bf16 maps it to 10); fp32 operands that do not allow 16-byte loads
+ * run on tiles 6, 8, 9, 10 with 4-byte lanes (11 and 12 map to 10), else at
+ * 128x128 or 64x64; bf16 ones at 128x128 or 64x64); "vec1"
  * (1 = force the narrow-load kernels); "splits" (0..4096, split-K count for
  * mt_linear_bwd's dw, 0 = automatic); "parts" (0..4096, row slices of the db
  * and broadcast-gradient reductions, 0 = automatic); "krot" (1 = the default:

@@ -152,9 +152,17 @@ int choose_cfg_aligned(int64_t M, int64_t N, int64_t batch, int64_t stages, bool
   // the 4-wave form (the 8-wave one is 3% slower on dX and dW there)
   const int mid = vec ? (bf16 ? mt::kCfgDma128x128 : mt::kCfgDma128x128w8)
                       : (bf16 ? mt::kCfg128x128 : mt::kCfgDma128x128);
+  // up to one tile per CU, fp32 with 16-byte loads: the 8-wave form at BK =
+  // 64 (one block per CU, half as many stages and barriers; on 4096 x 1024 x
+  // 1024: Y +1%, dX +2%, dW +5% split four ways against eight)
+  const int small = vec && !bf16 ? mt::kCfgDma128x128k64 : mid;
   const int64_t t128 = tiles(128, 128);
-  if (t128 >= 128) return mid;
-  if (can_split && t128 * std::min<int64_t>(16, stages / 8) >= 256) return mid;
+  if (t128 >= 128) return t128 <= 256 ? small : mid;
+  if (can_split && t128 * std::min<int64_t>(16, stages / 8) >= 256) {
+    // the BK = 64 form only where runs of at least 8 of its stages fill the CUs
+    const int64_t runs = t128 > 0 ? std::min<int64_t>(256 / t128, cdiv(K, 64) * red / 8) : 0;
+    return t128 * runs >= 256 ? small : mid;
+  }
   return mt::kCfg64x64;
 }
 
@@ -163,10 +171,12 @@ int choose_cfg_aligned(int64_t M, int64_t N, int64_t batch, int64_t stages, bool
 // run and at most 16 runs.
 int choose_splits(int64_t blocks, int64_t stages, int cfg) {
   if (g_force_splits > 0) return (int)std::min<int64_t>(g_force_splits, std::max<int64_t>(stages, 1));
-  if (cfg == mt::kCfgDma256x256) {
-    // one block per CU: runs that together fill the 256 CUs once
+  if (cfg == mt::kCfgDma256x256 || cfg == mt::kCfgDma128x128k64) {
+    // one block per CU: runs that together fill the 256 CUs once, each at
+    // least 1024 (256x256) or 512 (128x128 at BK = 64) deep in K
     if (blocks >= 256) return 1;
-    int64_t s = std::min<int64_t>(256 / blocks, stages / kDmaMinRunStages);
+    const int64_t min_run = cfg == mt::kCfgDma128x128k64 ? 8 : kDmaMinRunStages;
+    int64_t s = std::min<int64_t>(256 / blocks, stages / min_run);
     return s < 1 ? 1 : (int)s;
   }
   if (blocks >= 512) return 1;
@@ -235,6 +245,9 @@ size_t plan_gemm(GemmCall& g, bool may_split) {
                        g.vec, p.K, p.red_count);
   // the gathering convolution kernels exist on the DMA tiles 256x256 and 128x128
   if (g.conv && !mt::gemm_conv_cfg(g.cfg)) g.cfg = mt::kCfgDma128x128w8;
+  // the BK = 64 128x128 tile exists for fp32 with 16-byte lanes only
+  if (g.cfg == mt::kCfgDma128x128k64 && (g.bf16 || !g.vec))
+    g.cfg = g.bf16 ? mt::kCfgDma128x128 : mt::kCfgDma128x128w8;
   // operands or output without 16-byte aligned rows: fp32 keeps the DMA tiles
   // (4-byte lanes, element stores) and maps the register-staged tiles above
   // 128x128 to them; the element-load register-staged kernels stop at 128x128

@@ -107,13 +107,16 @@ struct DmaTile {
   static constexpr int BLOCKS = BYTES / 1024;          // 1 KB DMA blocks per stage
   static constexpr int EPC = 16 / ES;                   // elements per 16-byte chunk
   static_assert(BYTES % 1024 == 0, "tile must be whole 1 KB blocks");
-  static_assert(!KC || RB == 64 || RB == 128, "K-contiguous rows of 64 or 128 bytes");
+  static_assert(!KC || RB == 64 || RB == 128 || RB == 256, "K-contiguous rows of 64 to 256 bytes");
   static_assert(KC || RB >= 256, "M/N-contiguous rows of at least 256 bytes");
 
   static __device__ __forceinline__ int swz(int r) {
     if constexpr (KC) {
       if constexpr (RB == 64) return ((r >> 1) & 3) ^ ((r >> 3) & 1);
-      else return (r & 7) ^ ((r >> 3) & 1);
+      else if constexpr (RB == 128) return (r & 7) ^ ((r >> 3) & 1);
+      // 256-byte rows: 16 consecutive rows put one chunk in 16 distinct
+      // 16-byte slots of the 256-byte window
+      else return r & 15;
     } else if constexpr (ES == 2) {
       return 4 * (r & 3);
     } else {

@@ -61,6 +61,7 @@ static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream
       case kCfgDma128x256: return launch_dma<A_KC, B_KC, 128, 256, 16, 2, 2, 3, 2>(p, stream);
       case kCfgDma128x128: return launch_dma<A_KC, B_KC, 128, 128, 32, 2, 2, 2, 2>(p, stream);
       case kCfgDma128x128w8: return launch_dma<A_KC, B_KC, 128, 128, 32, 4, 2, 2, 4>(p, stream);
+      case kCfgDma128x128k64: return launch_dma<A_KC, B_KC, 128, 128, 64, 4, 2, 2, 2>(p, stream);
       case kCfg256x256: return launch_f32<A_KC, B_KC, 256, 256, 16, 2, 2, VEC, 1>(p, stream);
       case kCfg256x256x64w8: return launch_f32<A_KC, B_KC, 256, 256, 32, 2, 4, VEC, 2>(p, stream);
       case kCfg256x128: return launch_f32<A_KC, B_KC, 256, 128, 16, 2, 2, VEC, 2>(p, stream);
@@ -76,7 +77,7 @@ int gemm_tile_m(int cfg) {
     case kCfg256x256: case kCfg256x128: case kCfg256x256x64w8: case kCfgDma256x256:
     case kCfgDma256x256w4: case kCfgDma256x128: return 256;
     case kCfg128x256: case kCfg128x128: case kCfgDma128x256: case kCfgDma128x128:
-    case kCfgDma128x128w8: return 128;
+    case kCfgDma128x128w8: case kCfgDma128x128k64: return 128;
     default: return 64;
   }
 }
@@ -85,11 +86,12 @@ int gemm_tile_n(int cfg) {
     case kCfg256x256: case kCfg128x256: case kCfg256x256x64w8: case kCfgDma256x256:
     case kCfgDma256x256w4: case kCfgDma128x256: return 256;
     case kCfg256x128: case kCfg128x128: case kCfgDma256x128: case kCfgDma128x128:
-    case kCfgDma128x128w8: return 128;
+    case kCfgDma128x128w8: case kCfgDma128x128k64: return 128;
     default: return 64;
   }
 }
 int gemm_tile_k(int cfg, bool bf16) {
+  if (cfg == kCfgDma128x128k64) return 64;
   if (cfg == kCfg256x256x64w8) return bf16 ? 64 : 32;
   if (cfg == kCfgDma256x256 || cfg == kCfgDma256x256w4 || cfg == kCfgDma128x128 ||
       cfg == kCfgDma128x128w8)
