@@ -381,10 +381,27 @@ struct DmaMma<float, A_KC, B_KC, TM, TN, BK, BM, BN> {
       for (int j = 0; j < 4; ++j) f[j][i] = *(const float*)(S + Tl::addr(8 * g + 4 * h + j, mn));
     }
   }
+  // An M-contiguous A (TN products) is read TM consecutive rows at a time:
+  // tile i's row r is the wave's row TM r + i (ROW_PERM), so one TM-wide read
+  // of LDS row k feeds all TM tiles instead of TM 4-byte reads; the epilogue
+  // writes tile i's row r to that row.
+  static constexpr bool ROW_PERM = !A_KC && (TM == 2 || TM == 4);
+  typedef float f32xTM __attribute__((ext_vector_type(TM == 4 ? 4 : 2)));
   static __device__ __forceinline__ void load(const char* As, const char* Bs, int am, int bn,
                                               int lane, int g, Frags& f) {
+    if constexpr (ROW_PERM) {
+      using Tl = DmaTile<4, false, BM, BK>;
+      const int h = lane >> 5, c = am + TM * (lane & 31);
 #pragma unroll
-    for (int i = 0; i < TM; ++i) frag<A_KC, BM, TM>(As, am + i * 32, g, lane, f.a, i);
+      for (int j = 0; j < 4; ++j) {
+        const f32xTM v = *(const f32xTM*)(As + Tl::addr(8 * g + 4 * h + j, c));
+#pragma unroll
+        for (int i = 0; i < TM; ++i) f.a[j][i] = v[i];
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) frag<A_KC, BM, TM>(As, am + i * 32, g, lane, f.a, i);
+    }
 #pragma unroll
     for (int i = 0; i < TN; ++i) frag<B_KC, BN, TN>(Bs, bn + i * 32, g, lane, f.b, i);
   }
@@ -404,6 +421,7 @@ struct DmaMma<float, A_KC, B_KC, TM, TN, BK, BM, BN> {
 template <bool A_KC, bool B_KC, int TM, int TN, int BK, int BM, int BN>
 struct DmaMma<__bf16, A_KC, B_KC, TM, TN, BK, BM, BN> {
   static constexpr int KSTEPS = BK / 16;
+  static constexpr bool ROW_PERM = false;
   struct Frags {
     u16x8 a[TM], b[TN];
   };
