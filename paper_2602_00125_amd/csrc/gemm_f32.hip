@@ -60,7 +60,7 @@ static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream
       case kCfgDma256x128: return launch_dma<A_KC, B_KC, 256, 128, 16, 2, 2, 3, 2>(p, stream);
       case kCfgDma128x256: return launch_dma<A_KC, B_KC, 128, 256, 16, 2, 2, 3, 2>(p, stream);
       case kCfgDma128x128: return launch_dma<A_KC, B_KC, 128, 128, 32, 2, 2, 2, 2>(p, stream);
-      case kCfgDma128x128w8: return launch_dma<A_KC, B_KC, 128, 128, 32, 4, 2, 2, 4>(p, stream);
+      case kCfgDma128x128w8: return launch_dma<A_KC, B_KC, 128, 128, 32, 2, 4, 2, 4>(p, stream);
       case kCfgDma128x128k64: return launch_dma<A_KC, B_KC, 128, 128, 64, 2, 4, 2, 2>(p, stream);
       case kCfg256x256: return launch_f32<A_KC, B_KC, 256, 256, 16, 2, 2, VEC, 1>(p, stream);
       case kCfg256x256x64w8: return launch_f32<A_KC, B_KC, 256, 256, 32, 2, 4, VEC, 2>(p, stream);
@@ -141,7 +141,7 @@ static hipError_t conv_cfg(const GemmParams& p, int cfg, hipStream_t stream) {
   switch (cfg) {
     case kCfgDma256x256: return launch_conv<MODE, 256, 256, 32, 2, 4, 2, 2>(p, stream);
     case kCfgDma128x128: return launch_conv<MODE, 128, 128, 32, 2, 2, 2, 2>(p, stream);
-    case kCfgDma128x128w8: return launch_conv<MODE, 128, 128, 32, 4, 2, 2, 4>(p, stream);
+    case kCfgDma128x128w8: return launch_conv<MODE, 128, 128, 32, 2, 4, 2, 4>(p, stream);
     default: return hipErrorInvalidValue;
   }
 }

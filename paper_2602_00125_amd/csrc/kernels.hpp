@@ -24,7 +24,7 @@ enum GemmCfg {
   kCfgDma256x128 = 8,    // 256x128, 4 waves, BK = 16 / 32, 3-stage ring (72 KB), 2 blocks per CU
   kCfgDma128x256 = 9,    // 128x256, likewise
   kCfgDma128x128 = 10,   // 128x128, 4 waves, BK = 32 / 64, 2-stage ring (64 KB), 2 blocks per CU
-  kCfgDma128x128w8 = 11, // the same tile with 8 waves (32x64 each)
+  kCfgDma128x128w8 = 11, // the same tile with 8 waves (fp32: 64x32 each; bf16: 32x64)
   kCfgDma128x128k64 = 12, // fp32 only: 128x128, 8 waves of 64x32, BK = 64, 2-stage ring (128 KB), 1 block per CU
   kNumGemmCfg = 13
 };
