@@ -232,3 +232,26 @@ def test_generic_workspace_query_matches_the_per_op_ones():
     assert ws(b.OP["mse_loss"], P) == SIZE_MAX                      # wrong count
     assert ws(b.OP["matmul"], A, D([1, 8, 256, 383], ptr=0x10000000), C) == SIZE_MAX  # shape
     assert b.lib.mt_last_error()                                    # the reason is recorded
+
+
+def test_planner_split_decisions():
+    """The measured split-K rules, seen through the workspace queries (host
+    only): the 4096 x 1024 x 1024 layer runs dX whole (one 128x128 tile per
+    CU) and dW split four ways on the 64-deep 128x128 tile (4 x 1024 x 1024
+    partial floats); 8192^3 needs no split; a 256-row layer splits dX four
+    ways on the 8-wave 128x128 tile; db takes its row-slice partials."""
+    n = ctypes.c_size_t(0)
+    G = 1 << 32
+
+    def need(M, N, K, which):
+        x, w, dy = D([M, K], ptr=G), D([N, K], ptr=2 * G), D([M, N], ptr=3 * G)
+        outs = {"dx": D([M, K], ptr=4 * G), "dw": D([N, K], ptr=5 * G), "db": D([N], ptr=6 * G)}
+        args = [R(outs[k]) if k == which else None for k in ("dx", "dw", "db")]
+        assert b.lib.mt_linear_bwd_workspace(R(x), R(w), R(dy), *args, ctypes.byref(n)) == 0
+        return n.value
+
+    assert need(4096, 1024, 1024, "dx") == 0
+    assert need(4096, 1024, 1024, "dw") == 4 * 1024 * 1024 * 4
+    assert need(4096, 1024, 1024, "db") == 16 * 1024 * 4
+    assert need(8192, 8192, 8192, "dx") == 0 and need(8192, 8192, 8192, "dw") == 0
+    assert need(256, 1024, 4096, "dx") == 4 * 256 * 4096 * 4
