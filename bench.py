@@ -3,14 +3,15 @@
 
 One step = the whole hot path on one batch of synthetic inputs already in
 HBM: Y = X W^T + b (mt_linear_fwd), then dX = dY W, dW = dY^T X and
-db = 1^T dY (one mt_linear_bwd call). The step time comes from events
-around the timed steps; a second pass issues the same kernels with the
-backward split into one call per output, so that HIP events bracket each
-kernel for the roofline of the dominant one.
+db = 1^T dY (one mt_linear_bwd call). Events at every step boundary time
+each step; `value` comes from the median step (the mean is reported
+beside it). A second pass issues the same kernels with the backward split
+into one call per output, so that HIP events bracket each kernel for the
+roofline of the dominant one.
 
 Prints ONE JSON line: TFLOP/s of the three products (6 M N K flop per step)
-over the timed steps, the dominant kernel's roofline, and the fp64 CPU
-oracle timed on a bounded sample as a baseline.
+at the median step time, the dominant kernel's roofline, and the fp64 CPU
+oracle timed on full row bands of the step as a baseline.
 """
 from __future__ import annotations
 
@@ -85,55 +86,70 @@ def copy_probe(mib: int) -> None:
     print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4}))
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(inp, seconds: float):
-    """Time the fp64 oracle on a bounded random sample of the step's outputs."""
+    """Time the fp64 oracle on full row bands of the step: for each band of R
+    rows, Y and dX for R rows of X / dY and dW for R rows of dW (R columns of
+    dY), each through the oracle's row-major whole-matrix functions at full
+    contraction length; bands are taken until about `seconds` have passed."""
     import numpy as np
+    import torch
 
     import oracle
 
-    X = inp["X"].double().numpy() if inp["X"].dtype != __import__("torch").bfloat16 else None
-    if X is None:
-        to64 = lambda t: oracle.bf16_bits_to_f64(t.view(__import__("torch").int16).numpy())
-        X, W, dY = to64(inp["X"]), to64(inp["W"]), to64(inp["dY"])
-    else:
-        W, dY = inp["W"].double().numpy(), inp["dY"].double().numpy()
+    def f64(t):
+        if t.dtype == torch.bfloat16:
+            return oracle.bf16_bits_to_f64(t.view(torch.int16).numpy())
+        return t.double().numpy()
+
+    X, W, dY = f64(inp["X"]), f64(inp["W"]), f64(inp["dY"])
     B = inp["b"].double().numpy()
     M, K = X.shape
     N = W.shape[0]
-    rng = np.random.default_rng(0)
-    macs = 0
-    done = 0
+    R = 32
+    macs = bands = 0
     t0 = time.perf_counter()
-    chunk = 64
     while True:
-        r, c = rng.integers(0, M, chunk), rng.integers(0, N, chunk)
-        oracle.linear_fwd_at(X, W, B, r, c)
-        r, c = rng.integers(0, M, chunk), rng.integers(0, K, chunk)
-        oracle.linear_bwd_dx_at(dY, W, r, c)
-        r, c = rng.integers(0, N, chunk), rng.integers(0, K, chunk)
-        oracle.linear_bwd_dw_at(dY, X, r, c)
-        macs += chunk * (K + N + M)
-        done += chunk
-        el = time.perf_counter() - t0
-        if el >= seconds:
+        r0 = (bands * R) % max(M - R + 1, 1)
+        n0 = (bands * R) % max(N - R + 1, 1)
+        xb, gb = X[r0:r0 + R], dY[r0:r0 + R]
+        oracle.linear_fwd(xb, W, B)
+        oracle.linear_bwd_dx(gb, W)
+        oracle.linear_bwd_dw(np.ascontiguousarray(dY[:, n0:n0 + R]), X)
+        macs += len(xb) * N * K + len(gb) * N * K + R * M * K
+        bands += 1
+        if time.perf_counter() - t0 >= seconds:
             break
-        if el < seconds / 8:
-            chunk *= 2
     el = time.perf_counter() - t0
-    return {"value": 2.0 * macs / el / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": f"{done} random output elements of each of Y, dX, dW (full-length fp64 dot "
-                      f"products with the |a*b| bound) in {el:.1f} s; TFLOP/s = 2*MACs/s"}
+    flops = 2.0 * macs / el
+    return {"value": flops / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle", "gflops": round(flops / 1e9, 3), "cpu_model": cpu_model(),
+            "sample": f"row band: {bands} bands of {R} rows, each {R} full rows of Y = X W^T + b "
+                      f"and of dX = dY W and {R} full rows of dW = dY^T X (the oracle's row-major "
+                      f"fp64 functions with the |a*b| bound, full contraction length) in {el:.1f} s; "
+                      f"TFLOP/s = 2*MACs/s"}
 
 
 WARMUP_USED = [None]  # warm-up steps of the run's timed pass (reported as "warmup")
 
 
 def timed_steps(step, n_events: int, steps: int, warmup: int):
-    """Warm up, then time `steps` steps (events between their calls when
-    n_events > 1); returns (mean ms per step, mean ms between events).
-    warmup < 0: steps, each waited for, until about a second has passed (at
-    least 5)."""
+    """Warm up, then time `steps` steps, bracketed by synchronisations, with an
+    event at every step boundary (and events between a step's calls when
+    n_events > 1). Returns (median ms per step, mean ms between each step's
+    events, mean ms per step). warmup < 0: steps, each waited for, until
+    about a second has passed (at least 5)."""
+    import statistics
+
     import torch
 
     if warmup < 0:
@@ -148,23 +164,23 @@ def timed_steps(step, n_events: int, steps: int, warmup: int):
             step()
     if WARMUP_USED[0] is None:  # the first call is the timed pass of the run
         WARMUP_USED[0] = warmup
-    torch.cuda.synchronize()
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(n_events)] for _ in range(steps)]
     if n_events < 2:
         events = [None] * steps
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
+    bounds = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     torch.cuda.synchronize()
-    t0.record()
     for i in range(steps):
+        bounds[i].record()
         step(events[i])
-    t1.record()
+    bounds[steps].record()
     torch.cuda.synchronize()
+    per_step = [bounds[i].elapsed_time(bounds[i + 1]) for i in range(steps)]
     per = [0.0] * max(n_events - 1, 0)
     for ev in events:
         for j in range(n_events - 1):
             per[j] += ev[j].elapsed_time(ev[j + 1])
-    return t0.elapsed_time(t1) / steps, [v / steps for v in per]
+    mean = bounds[0].elapsed_time(bounds[steps]) / steps
+    return statistics.median(per_step), [v / steps for v in per], mean
 
 
 def bench_bmm(args, w, inp, dev):
@@ -196,7 +212,7 @@ def bench_bmm(args, w, inp, dev):
         if ev is not None:
             ev[3].record()
 
-    ms, per = timed_steps(step, 4, args.steps, args.warmup)
+    ms, per, ms_mean = timed_steps(step, 4, args.steps, args.warmup)
     names = ["fwd_gemm", "dA_gemm_reduce_into", "dB_gemm_reduce_into"]
     per = dict(zip(names, per))
     value = w.flops() / (ms * 1e-3) / 1e12
@@ -204,7 +220,7 @@ def bench_bmm(args, w, inp, dev):
     achieved = (w.flops() / 3) / (per[dominant] * 1e-3) / 1e12
     out = {"metric": f"TFLOP/s for broadcast matmul fwd+bwd (3 products) on {args.workload}",
            "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
-           "warmup": WARMUP_USED[0], "ms_per_step": round(ms, 4), "higher_is_better": True,
+           "warmup": WARMUP_USED[0], "ms_per_step": round(ms, 4), "ms_per_step_mean": round(ms_mean, 4), "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
            "config": {"workload": args.workload, "a": list(w.ashape), "b": list(w.bshape),
                       "pct_of_mfma_peak": round(100.0 * value / FP32_MFMA_PEAK_TFLOPS, 2)},
@@ -303,8 +319,8 @@ def bench_mlp(args, w, inp, dev):
 
     names = ["fwd1_nt_gemm_gelu", "fwd2_nt_gemm", "mse", "dh1_nn_gemm", "dw2_tn_gemm",
              "db2_colsum", "act_bwd_db1", "dw1_tn_gemm", "adam"]
-    ms_step, _ = timed_steps(step, 1, args.steps, args.warmup)
-    _, per = timed_steps(step, len(names) + 1, args.steps, 1)
+    ms_step, _, ms_mean = timed_steps(step, 1, args.steps, args.warmup)
+    _, per, _ = timed_steps(step, len(names) + 1, args.steps, 1)
     per = dict(zip(names, per))
     value = w.flops() / (ms_step * 1e-3) / 1e12
     gemm_flops = {"fwd1_nt_gemm_gelu": 2.0 * M * w.D0 * D1, "fwd2_nt_gemm": 2.0 * M * D1 * D2,
@@ -321,7 +337,7 @@ def bench_mlp(args, w, inp, dev):
     out = {"metric": f"TFLOP/s for a two-layer perceptron training step (5 GEMMs + GELU, MSE, "
                      f"Adam) on {args.workload}",
            "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
-           "warmup": WARMUP_USED[0], "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+           "warmup": WARMUP_USED[0], "ms_per_step": round(ms_step, 4), "ms_per_step_mean": round(ms_mean, 4), "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
            "config": {"workload": args.workload, "M": M, "D0": w.D0, "D1": D1, "D2": D2,
                       "act": w.act, "optimizer": "adam",
@@ -405,13 +421,13 @@ def bench_conv(args, w, inp, dev):
         if ev is not None:
             ev[2].record()
 
-    ms, _ = timed_steps(step, 1, args.steps, args.warmup)
-    _, per = timed_steps(step, 3, args.steps, 1)
+    ms, _, ms_mean = timed_steps(step, 1, args.steps, args.warmup)
+    _, per, _ = timed_steps(step, 3, args.steps, 1)
     per = dict(zip(["conv2d_fwd", "conv2d_bwd"], per))
     value = w.flops() / (ms * 1e-3) / 1e12
     out = {"metric": f"TFLOP/s for a 2-D convolution fwd+bwd (3 products) on {args.workload}",
            "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
-           "warmup": WARMUP_USED[0], "ms_per_step": round(ms, 4), "higher_is_better": True,
+           "warmup": WARMUP_USED[0], "ms_per_step": round(ms, 4), "ms_per_step_mean": round(ms_mean, 4), "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
            "config": {"workload": args.workload, "x": [w.N, w.C, w.H, w.W],
                       "w": [w.CO, w.C, w.KH, w.KW], "stride": list(st), "pad": list(pd),
@@ -496,11 +512,9 @@ def main():
 
         def run(ev=None):
             graph.replay()
-    total_ms_step, _ = timed_steps(run, 1, args.steps, args.warmup)
-    _, per_list = timed_steps(step_per_kernel, 5, args.steps, 1)
+    ms_per_step, _, ms_mean = timed_steps(run, 1, args.steps, args.warmup)
+    _, per_list, _ = timed_steps(step_per_kernel, 5, args.steps, 1)
     per = dict(zip(["fwd_nt_gemm", "dx_nn_gemm", "dw_tn_gemm", "db_colsum"], per_list))
-    total_ms = total_ms_step * args.steps
-    ms_per_step = total_ms / args.steps
     flops = w.flops()
     value = flops / (ms_per_step * 1e-3) / 1e12
     gemm_flops = 2.0 * M * N * K
@@ -530,6 +544,7 @@ def main():
         "steps": args.steps,
         "warmup": WARMUP_USED[0],
         "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step_mean": round(ms_mean, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

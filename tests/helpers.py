@@ -52,3 +52,28 @@ def sample_positions(rows: int, cols: int, n_random: int, seed: int = 0, tile=25
     r = np.concatenate([r, rng.integers(0, rows, n_random)])
     c = np.concatenate([c, rng.integers(0, cols, n_random)])
     return r.astype(np.int64), c.astype(np.int64)
+
+
+def hip_runtime_loads() -> bool:
+    """Whether the HIP runtime library can be loaded on this host (it can on
+    any ROCm install, GPU or not; only then is the C-ABI library loadable)."""
+    import ctypes
+
+    try:
+        ctypes.CDLL("libamdhip64.so")
+        return True
+    except OSError:
+        return False
+
+
+def load_binding():
+    """The ctypes binding. Where the HIP runtime loads, a missing or broken
+    library is an error (never a skip); without a HIP runtime the host-ABI
+    checks are skipped."""
+    import pytest
+
+    if not hip_runtime_loads():
+        pytest.skip("libamdhip64 does not load on this host", allow_module_level=True)
+    from paper_2602_00125_amd import binding
+
+    return binding

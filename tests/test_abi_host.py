@@ -11,11 +11,12 @@ import numpy as np
 import pytest
 
 import oracle
+from helpers import load_binding
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "minitensor_hip.h")
 
-b = pytest.importorskip("paper_2602_00125_amd.binding")
+b = load_binding()
 
 
 def test_exports_every_declared_symbol():

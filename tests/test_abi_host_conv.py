@@ -6,7 +6,9 @@ import ctypes
 
 import pytest
 
-b = pytest.importorskip("paper_2602_00125_amd.binding")
+from helpers import load_binding
+
+b = load_binding()
 
 from test_abi_host import BF16, D, R  # noqa: E402
 
