@@ -123,6 +123,27 @@ mt_status mt_linear_bwd_workspace(const mt_tensor* x, const mt_tensor* w, const 
                                   const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db,
                                   size_t* bytes);
 
+/* mt_linear_bwd_noalloc: mt_linear_bwd for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc). It takes no workspace: the split-K partials and db
+ * row-slice sums go to a fixed scratch array inside the library, one per GPU
+ * (MT_NOALLOC_SCRATCH_BYTES, held from the first call on that GPU until the
+ * process ends). The call allocates nothing; it runs the same kernels with
+ * the same plan as mt_linear_bwd given a workspace of the size
+ * mt_linear_bwd_workspace reports, so the results are bit-identical to that.
+ *   Arguments, flags and errors as mt_linear_bwd; in addition
+ *   MT_ERR_WORKSPACE (nothing enqueued) when these sizes need more scratch
+ *   than MT_NOALLOC_SCRATCH_BYTES, and MT_ERR_INVALID when `stream` does not
+ *   belong to the current device.
+ *   Every call on one GPU shares that GPU's scratch array: calls that overlap
+ *   in time on one GPU (other streams, other threads) race and must be
+ *   ordered by the caller. Nothing in the array needs to start at zero.
+ */
+#define MT_NOALLOC_SCRATCH_BYTES (32u << 20)
+mt_status mt_linear_bwd_noalloc(const mt_tensor* x, const mt_tensor* w, const mt_tensor* dy,
+                                const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db,
+                                uint32_t flags, void* stream);
+
 /* ------------------------------------------ dense layer + nonlinearity
  * Nonlinearities of Sec. 3.3 ("Nonlinearities"): ReLU, Sigmoid, Tanh, GELU
  * (z Phi(z) with the standard normal CDF Phi, not its tanh approximation).

@@ -33,7 +33,8 @@ EXPORTS = ["mt_linear_fwd", "mt_linear_bwd", "mt_linear_bwd_workspace", "mt_matm
            "mt_linear_act_fwd", "mt_act_bwd", "mt_act_bwd_workspace", "mt_mse_loss",
            "mt_mse_loss_workspace", "mt_sgd_step", "mt_adam_step", "mt_rmsprop_step",
            "mt_conv2d_fwd", "mt_conv2d_fwd_workspace", "mt_conv2d_bwd", "mt_conv2d_bwd_workspace",
-           "mt_workspace_bytes"]
+           "mt_workspace_bytes", "mt_linear_bwd_noalloc"]
+NOALLOC_SCRATCH_BYTES = 32 << 20  # MT_NOALLOC_SCRATCH_BYTES
 ACT = {"none": 0, "relu": 1, "sigmoid": 2, "tanh": 3, "gelu": 4}
 
 
@@ -48,6 +49,7 @@ _I64P = ctypes.POINTER(ctypes.c_int64)
 lib.mt_linear_fwd.argtypes = [_P, _P, _P, _P, _vp]
 lib.mt_linear_bwd.argtypes = [_P, _P, _P, _P, _P, _P, _u32, _vp, _sz, _vp]
 lib.mt_linear_bwd_workspace.argtypes = [_P, _P, _P, _P, _P, _P, ctypes.POINTER(_sz)]
+lib.mt_linear_bwd_noalloc.argtypes = [_P, _P, _P, _P, _P, _P, _u32, _vp]
 lib.mt_matmul.argtypes = [_P, _P, _P, _u32, _vp, _sz, _vp]
 lib.mt_matmul_workspace.argtypes = [_P, _P, _P, _u32, ctypes.POINTER(_sz)]
 lib.mt_reduce_broadcast_grad.argtypes = [_P, _P, _u32, _vp, _sz, _vp]
@@ -166,6 +168,14 @@ def linear_bwd(x, w, dy, dx=None, dw=None, db=None, accumulate=False, workspace=
     ptr, nbytes = _ws(workspace)
     _check(lib.mt_linear_bwd(*[_ref(d) for d in ds], ACCUMULATE if accumulate else 0, ptr, nbytes,
                              _stream(stream)), "mt_linear_bwd")
+
+
+def linear_bwd_noalloc(x, w, dy, dx=None, dw=None, db=None, accumulate=False,
+                       stream=None) -> None:
+    """linear_bwd with the library's own scratch array as its workspace."""
+    ds = [desc(t) for t in (x, w, dy, dx, dw, db)]
+    _check(lib.mt_linear_bwd_noalloc(*[_ref(d) for d in ds], ACCUMULATE if accumulate else 0,
+                                     _stream(stream)), "mt_linear_bwd_noalloc")
 
 
 def matmul_workspace(a, b, c, accumulate=False, reduce_into=False) -> int:

@@ -17,7 +17,7 @@ OUT = os.path.join(HERE, "libminitensor_hip.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["gemm_f32.hip", "gemm_bf16.hip", "reduce.hip", "elementwise.hip", "conv.hip",
+SOURCES = ["gemm_f32.hip", "gemm_bf16.hip", "reduce.hip", "elementwise.hip", "conv.hip", "noalloc.hip",
            "shape.cpp", "capi.cpp", "conv_host.cpp"]
 COMMON = ["-std=c++17", "-O3", "-fPIC", "-Wall", "-Wno-unused-result",
           f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
