@@ -306,9 +306,8 @@ def bench_mlp(args, w, inp, dev):
         else:
             mt.linear_bwd(h1, W2, dp, dh1, None, None, workspace=ws)
             mark()
-            mt.linear_bwd(h1, W2, dp, None, grads[2], None, workspace=ws)
-            mark()
-            mt.linear_bwd(h1, W2, dp, None, None, grads[3], workspace=ws)
+            # db2 is summed inside the dW2 product
+            mt.linear_bwd(h1, W2, dp, None, grads[2], grads[3], workspace=ws)
         mark()
         mt.act_bwd(w.act, z1, dh1, dz1, grads[1], workspace=ws)
         mark()
@@ -317,20 +316,20 @@ def bench_mlp(args, w, inp, dev):
         mt.adam_step(params, grads, ms, vs, 1e-4, 0.9, 0.999, 1e-8, counter[0])
         mark()
 
-    names = ["fwd1_nt_gemm_gelu", "fwd2_nt_gemm", "mse", "dh1_nn_gemm", "dw2_tn_gemm",
-             "db2_colsum", "act_bwd_db1", "dw1_tn_gemm", "adam"]
+    names = ["fwd1_nt_gemm_gelu", "fwd2_nt_gemm", "mse", "dh1_nn_gemm", "dw2_tn_gemm_db2",
+             "act_bwd_db1", "dw1_tn_gemm", "adam"]
     ms_step, _, ms_mean = timed_steps(step, 1, args.steps, args.warmup)
     _, per, _ = timed_steps(step, len(names) + 1, args.steps, 1)
     per = dict(zip(names, per))
     value = w.flops() / (ms_step * 1e-3) / 1e12
     gemm_flops = {"fwd1_nt_gemm_gelu": 2.0 * M * w.D0 * D1, "fwd2_nt_gemm": 2.0 * M * D1 * D2,
-                  "dh1_nn_gemm": 2.0 * M * D2 * D1, "dw2_tn_gemm": 2.0 * M * D2 * D1,
+                  "dh1_nn_gemm": 2.0 * M * D2 * D1, "dw2_tn_gemm_db2": 2.0 * M * D2 * D1,
                   "dw1_tn_gemm": 2.0 * M * D1 * w.D0}
     dominant = max(gemm_flops, key=lambda k: per[k])
     achieved = gemm_flops[dominant] / (per[dominant] * 1e-3) / 1e12
     nparam = sum(p.numel() for p in params)
     hbm_bytes = {"act_bwd_db1": 12.0 * M * D1 + 4 * D1, "mse": 12.0 * M * D2 + 4,
-                 "adam": 28.0 * nparam, "db2_colsum": 4.0 * M * D2 + 4 * D2}
+                 "adam": 28.0 * nparam}
     hbm = {k: {"ms": round(per[k], 4), "gbs": round(v / (per[k] * 1e-3) / 1e9, 1),
                "frac": round(v / (per[k] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "bytes": int(v)}
            for k, v in hbm_bytes.items()}
@@ -480,8 +479,8 @@ def main():
         mt.linear_bwd(x, wt, dy, dx, dw, db, workspace=ws)
 
     def step_per_kernel(ev=None):
-        # the same kernels, the backward issued one output at a time so that
-        # events bracket each kernel
+        # the same kernels, the backward issued as two calls so that events
+        # bracket each product (db is summed inside the dW product)
         if ev is not None:
             ev[0].record()
         mt.linear_fwd(x, wt, bias, y)
@@ -490,12 +489,20 @@ def main():
         mt.linear_bwd(x, wt, dy, dx, None, None, workspace=ws)
         if ev is not None:
             ev[2].record()
-        mt.linear_bwd(x, wt, dy, None, dw, None, workspace=ws)
+        mt.linear_bwd(x, wt, dy, None, dw, db, workspace=ws)
         if ev is not None:
             ev[3].record()
-        mt.linear_bwd(x, wt, dy, None, None, db, workspace=ws)
+
+    # the stand-alone column sum (db without dw), for its HBM rate
+    ws_db_bytes = mt.linear_bwd_workspace(x, wt, dy, None, None, db)
+    ws_db = torch.empty(ws_db_bytes // 4 + 64, device=dev) if ws_db_bytes else None
+
+    def colsum_alone(ev=None):
         if ev is not None:
-            ev[4].record()
+            ev[0].record()
+        mt.linear_bwd(x, wt, dy, None, None, db, workspace=ws_db)
+        if ev is not None:
+            ev[1].record()
 
     run = step
     if args.graph:
@@ -513,14 +520,15 @@ def main():
         def run(ev=None):
             graph.replay()
     ms_per_step, _, ms_mean = timed_steps(run, 1, args.steps, args.warmup)
-    _, per_list, _ = timed_steps(step_per_kernel, 5, args.steps, 1)
-    per = dict(zip(["fwd_nt_gemm", "dx_nn_gemm", "dw_tn_gemm", "db_colsum"], per_list))
+    _, per_list, _ = timed_steps(step_per_kernel, 4, args.steps, 1)
+    per = dict(zip(["fwd_nt_gemm", "dx_nn_gemm", "dw_tn_gemm_db"], per_list))
+    _, cs_list, _ = timed_steps(colsum_alone, 2, args.steps, 1)
     flops = w.flops()
     value = flops / (ms_per_step * 1e-3) / 1e12
     gemm_flops = 2.0 * M * N * K
     is_bf16 = w.dtype == "bf16"
     peak = BF16_MFMA_PEAK_TFLOPS if is_bf16 else FP32_MFMA_PEAK_TFLOPS
-    dominant = max(("fwd_nt_gemm", "dx_nn_gemm", "dw_tn_gemm"), key=lambda k: per[k])
+    dominant = max(("fwd_nt_gemm", "dx_nn_gemm", "dw_tn_gemm_db"), key=lambda k: per[k])
     achieved = gemm_flops / (per[dominant] * 1e-3) / 1e12
     # HBM traffic of the dominant kernel from committed rocprofv3 counters, if
     # they were taken on the current kernel sources
@@ -558,7 +566,8 @@ def main():
                      "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
                      "traffic": traffic},
         "kernels_ms": {k: round(v, 4) for k, v in per.items()},
-        "db_colsum_gbs": round(db_bytes / (per["db_colsum"] * 1e-3) / 1e9, 1),
+        "colsum_alone": {"ms": round(cs_list[0], 4),
+                         "gbs": round(db_bytes / (cs_list[0] * 1e-3) / 1e9, 1), "bytes": db_bytes},
     }
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)

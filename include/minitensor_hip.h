@@ -113,6 +113,9 @@ mt_status mt_linear_fwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
  * ws/ws_bytes: optional workspace (size from mt_linear_bwd_workspace); used
  * for split reductions of db and split-K partial sums of dx / dw when their
  * output tiles under-fill the GPU.
+ * With dw and db both requested, db is summed inside the dW product from the
+ * dY tiles it reads (db is the column sum of that product's left operand
+ * dY^T), so dY is streamed once; db alone runs a column-sum pass over dY.
  */
 mt_status mt_linear_bwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* dy,
                         const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db,

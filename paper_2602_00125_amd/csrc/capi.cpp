@@ -233,6 +233,20 @@ bool vec_ok_operand(const void* base, int64_t rows_other, int64_t contig_extent,
 
 int vec_elems(bool bf16) { return bf16 ? 8 : 4; }
 
+// Whether the launcher runs tile configuration cfg on the DMA-ring kernel
+// (gemm_f32.hip / gemm_bf16.hip): bf16 only with 16-byte loads, fp32 with
+// 4-byte lanes on 256x256, 256x128, 128x256 and the 4-wave 128x128.
+bool dma_kernel(int cfg, bool vec, bool bf16) {
+  if (cfg < mt::kCfgDma256x256) return false;
+  if (vec) return true;
+  return !bf16 && (cfg == mt::kCfgDma256x256 || cfg == mt::kCfgDma256x128 ||
+                   cfg == mt::kCfgDma128x256 || cfg == mt::kCfgDma128x128);
+}
+
+// Byte offset of the split runs' column sums of A in the workspace: after
+// the partial tiles, 256-byte aligned.
+size_t colsum_part_offset(size_t tiles_bytes) { return (tiles_bytes + 255) & ~(size_t)255; }
+
 // Resolves the tile configuration, vector width and split-K of a product.
 // Returns the workspace bytes the split needs (0 = no split). With
 // ws_bytes < that, the product runs unsplit.
@@ -262,6 +276,11 @@ size_t plan_gemm(GemmCall& g, bool may_split) {
       g.cfg = mt::kCfg128x128;
     }
   }
+  // the column sums of A fold into the DMA kernels of plain TN products only
+  if (p.colsum && (g.a_kc || g.conv || p.nred > 0 || p.keep_count != 1 ||
+                   !dma_kernel(g.cfg, g.vec, g.bf16)))
+    p.colsum = nullptr;
+  p.colsum_part = nullptr;
   const int64_t stages = cdiv(p.K, mt::gemm_tile_k(g.cfg, g.bf16)) * p.red_count;
   p.splits = 1;
   p.stages_per_split = stages > 0 ? stages : 1;
@@ -299,7 +318,10 @@ size_t plan_gemm(GemmCall& g, bool may_split) {
   p.splits = (int32_t)splits;
   p.stages_per_split = per;
   p.partial_stride = p.keep_count * p.M * p.N;
-  return (size_t)splits * p.partial_stride * sizeof(float);
+  const size_t tiles_bytes = (size_t)splits * p.partial_stride * sizeof(float);
+  // the runs' column sums of A follow the partial tiles
+  return p.colsum ? colsum_part_offset(tiles_bytes) + (size_t)splits * p.M * sizeof(float)
+                  : tiles_bytes;
 }
 
 mt_status launch_gemm(GemmCall& g, hipStream_t stream, void* ws, size_t ws_bytes) {
@@ -311,6 +333,9 @@ mt_status launch_gemm(GemmCall& g, hipStream_t stream, void* ws, size_t ws_bytes
     p.partial = (float*)ws;
   } else if (need > 0 && need <= ws_bytes) {
     p.partial = (float*)ws;
+    if (p.colsum)
+      p.colsum_part = (float*)((char*)ws + colsum_part_offset((size_t)p.splits * p.partial_stride *
+                                                              sizeof(float)));
   } else {
     p.splits = 1;
     const int64_t stages = cdiv(p.K, mt::gemm_tile_k(g.cfg, g.bf16)) * p.red_count;
@@ -333,6 +358,10 @@ mt_status launch_gemm(GemmCall& g, hipStream_t stream, void* ws, size_t ws_bytes
     e = mt::splitk_finish(p.partial, p.splits, p.keep_count * p.M, p.N, p.c, p.ldc, p.bias,
                           p.accumulate != 0, stream);
     if (e != hipSuccess) return hip_status(e);
+    if (p.colsum) {
+      e = mt::parts_finish(p.colsum_part, p.splits, p.M, p.colsum, p.accumulate != 0, stream);
+      if (e != hipSuccess) return hip_status(e);
+    }
   }
   return MT_OK;
 }
@@ -419,6 +448,7 @@ mt_status linear_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tenso
   // dx / dw split-K partials and db row-slice sums
   GemmCall gdx{}, gdw{};
   size_t need_dx = 0, need_dw = 0, need_db = 0;
+  bool fold_db = false;
   if (dx && M > 0 && K > 0) {
     init_params(&gdx.p);
     gdx.p.a = dy->data;
@@ -460,13 +490,19 @@ mt_status linear_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tenso
               vec_ok_operand(x->data, M, K, gdw.p.ldb, nullptr, 0, per) &&
               aligned16(dw->data) && K % 4 == 0 && gdw.p.ldc % 4 == 0;
     gdw.cfg = -1;
+    // db = 1^T dY is the column sum of A = dY^T: folded into the dW product
+    // where its kernel allows (no second pass over dY)
+    // (whether it does is settled by the plan of the launch, below: without
+    // a workspace the product may take a tile that cannot)
+    gdw.p.colsum = db ? (float*)db->data : nullptr;
     GemmCall probe = gdw;
     need_dw = plan_gemm(probe, true);
+    fold_db = probe.p.colsum != nullptr;
   }
   int parts = 1;
   if (db && N > 0) {
     parts = g_force_parts > 0 ? g_force_parts : mt::colsum_parts(M, N);
-    if (parts > 1) need_db = (size_t)parts * N * sizeof(float);
+    if (parts > 1 && !fold_db) need_db = (size_t)parts * N * sizeof(float);
   }
   if (ws_query) {
     *ws_query = std::max(need_dx, std::max(need_dw, need_db));
@@ -478,12 +514,15 @@ mt_status linear_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tenso
   if (dx && M > 0 && K > 0) {
     if ((s = launch_gemm(gdx, stream, ws, ws_bytes))) return s;
   }
+  fold_db = false;
   if (dw && N > 0 && K > 0) {
     if ((s = launch_gemm(gdw, stream, ws, ws_bytes))) return s;
+    fold_db = gdw.p.colsum != nullptr;  // the product summed db itself
   }
-  if (db && N > 0) {
+  if (db && N > 0 && !fold_db) {
     (void)hipGetLastError();
-    float* wsp = (ws && parts > 1 && ws_bytes >= need_db) ? (float*)ws : nullptr;
+    const bool room = ws_bytes >= (size_t)parts * N * sizeof(float);
+    float* wsp = (ws && parts > 1 && room) ? (float*)ws : nullptr;
     hipError_t e = mt::colsum(dy->data, bf, M, N, pitch(dy), (float*)db->data, acc,
                               wsp, parts, stream);
     if (e != hipSuccess) return hip_status(e);

@@ -405,6 +405,17 @@ struct DmaMma<float, A_KC, B_KC, TM, TN, BK, BM, BN> {
 #pragma unroll
     for (int i = 0; i < TN; ++i) frag<B_KC, BN, TN>(Bs, bn + i * 32, g, lane, f.b, i);
   }
+  // Column sums of an M-contiguous A over the k-step's 4 MFMA steps: tile
+  // i's value goes to the lane's column (see a_col), lane half h holding k
+  // = 8g + 4h + j.
+  static __device__ __forceinline__ void colsum(const Frags& f, float (&cs)[TM]) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) cs[i] += (f.a[0][i] + f.a[1][i]) + (f.a[2][i] + f.a[3][i]);
+  }
+  // the column of A (from the wave's first) whose values tile i holds in this lane
+  static __device__ __forceinline__ int a_col(int lane, int i) {
+    return ROW_PERM ? TM * (lane & 31) + i : 32 * i + (lane & 31);
+  }
   // a k-step's MFMAs in 4 chunks: chunk j is MFMA step j of every tile
   static constexpr int CHUNKS = 4;
   static __device__ __forceinline__ void compute_chunk(const Frags& f, f32x16 (&acc)[TM][TN],
@@ -458,6 +469,25 @@ struct DmaMma<__bf16, A_KC, B_KC, TM, TN, BK, BM, BN> {
 #pragma unroll
     for (int i = 0; i < TN; ++i) f.b[i] = frag<B_KC, BN>(Bs, bn + i * 32, k0, lane);
   }
+  // Column sums of an M-contiguous A over the k-step: lane L of tile i
+  // holds 8 consecutive k of column 32 i + (L & 31), summed in pairs by
+  // v_dot2_f32_bf16 against (1, 1) (exact products, fp32 sums).
+  static __device__ __forceinline__ void colsum(const Frags& f, float (&cs)[TM]) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const bf16x2 one = __builtin_bit_cast(bf16x2, (uint32_t)0x3f803f80u);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      float s = cs[i];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        // elements 2e and 2e+1, packed as they sit in one register
+        const uint32_t pair = (uint32_t)f.a[i][2 * e] | ((uint32_t)f.a[i][2 * e + 1] << 16);
+        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pair), one, s, false);
+      }
+      cs[i] = s;
+    }
+  }
+  static __device__ __forceinline__ int a_col(int lane, int i) { return 32 * i + (lane & 31); }
   // a k-step's MFMAs in TM chunks: chunk i is row i of the wave's tiles
   static constexpr int CHUNKS = TM;
   static __device__ __forceinline__ void compute_chunk(const Frags& f, f32x16 (&acc)[TM][TN],

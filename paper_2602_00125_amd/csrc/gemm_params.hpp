@@ -97,6 +97,13 @@ struct GemmParams {
   // convolution kernels only: the gathered operand (A of the forward product,
   // B of the weight gradient); every other kernel ignores it
   ConvGather cg;
+  // DMA kernels with an M-contiguous A (TN products), no batch: the column
+  // sums of A over k, sum_k A[m][k], formed from the fragments the product
+  // already reads (the dense layer's db = 1^T dY, with A = dY^T). Unsplit,
+  // colsum[m] (+)= the sum (p.accumulate); split-K run s writes its sum to
+  // colsum_part[s * M + m] and the host adds the runs in order. Null: off.
+  float* colsum;
+  float* colsum_part;
 };
 
 }  // namespace mt

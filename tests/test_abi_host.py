@@ -254,5 +254,11 @@ def test_planner_split_decisions():
     assert need(4096, 1024, 1024, "dx") == 0
     assert need(4096, 1024, 1024, "dw") == 4 * 1024 * 1024 * 4
     assert need(4096, 1024, 1024, "db") == 16 * 1024 * 4
+    # dw with db: db is summed inside the split dW product, one sum of the
+    # 1024 columns per run after the (256-byte aligned) partial tiles
+    x, w, dy = D([4096, 1024], ptr=G), D([1024, 1024], ptr=2 * G), D([4096, 1024], ptr=3 * G)
+    assert b.lib.mt_linear_bwd_workspace(R(x), R(w), R(dy), None, R(D([1024, 1024], ptr=5 * G)),
+                                         R(D([1024], ptr=6 * G)), ctypes.byref(n)) == 0
+    assert n.value == 4 * 1024 * 1024 * 4 + 4 * 1024 * 4
     assert need(8192, 8192, 8192, "dx") == 0 and need(8192, 8192, 8192, "dw") == 0
     assert need(256, 1024, 4096, "dx") == 4 * 256 * 4096 * 4

@@ -143,3 +143,32 @@ def test_bf16_broadcast_matmul(seed):
     dAr, SA, dBr, SB = oracle.matmul_bwd(An, Bn, dCn)
     check_bf16(to_f64(dA), dAr, SA, "dA")
     check_bf16(to_f64(dB), dBr, SB, "dB")
+
+
+@pytest.mark.parametrize("cfg", [6, 7, 8, 9, 10, 11])
+@pytest.mark.parametrize("splits", [0, 3])
+def test_bf16_db_folded_into_dw(cfg, splits):
+    """bf16 dY: db summed inside the dW product (pairs of bf16 elements added
+    by v_dot2_f32_bf16 against ones: exact products, fp32 sums), whole and
+    split along the contraction."""
+    M, N, K = 520, 392, 264
+    inp = make(M, N, K, seed=41)
+    x, w, dy = (inp[k].to(DEV) for k in ("X", "W", "dY"))
+    dw = torch.full((N, K), float("nan"), device=DEV)
+    db = torch.full((N,), float("nan"), device=DEV)
+    b.debug_set("cfg", cfg)
+    b.debug_set("splits", splits)
+    try:
+        need = b.linear_bwd_workspace(x, w, dy, None, dw, db)
+        if splits:
+            need_dw = b.linear_bwd_workspace(x, w, dy, None, dw, None)
+            assert need == ((need_dw + 255) // 256) * 256 + splits * N * 4
+        ws = torch.empty(need // 4 + 64, device=DEV) if need else None
+        b.linear_bwd(x, w, dy, None, dw, db, workspace=ws)
+        torch.cuda.synchronize()
+    finally:
+        b.debug_set("cfg", -1)
+        b.debug_set("splits", 0)
+    X, dY = to_f64(inp["X"]), to_f64(inp["dY"])
+    check_bf16(to_f64(db), *oracle.linear_bwd_db(dY), "db")
+    check_bf16(to_f64(dw), *oracle.linear_bwd_dw(dY, X), "dW")

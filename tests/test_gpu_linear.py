@@ -223,3 +223,48 @@ def test_linear_zero_k_and_empty():
     out0 = run_linear(inp0)
     assert torch.equal(out0["dW"].cpu(), torch.zeros(3, 4))
     assert torch.equal(out0["db"].cpu(), torch.zeros(3))
+
+
+# DMA tiles (cfg, 4-byte lanes) whose weight-gradient product sums db itself
+FOLD_CFGS = [(6, 0), (6, 1), (7, 0), (8, 0), (8, 1), (9, 0), (9, 1), (10, 0), (10, 1), (11, 0),
+             (12, 0)]
+
+
+@pytest.mark.parametrize("cfg,vec1", FOLD_CFGS)
+@pytest.mark.parametrize("splits", [0, 3])
+@pytest.mark.parametrize("shape", [(520, 392, 264), (576, 320, 256)])
+def test_linear_db_folded_into_dw(cfg, vec1, splits, shape):
+    """db = 1^T dY summed inside the dW product from the dY tiles it already
+    reads (no second pass over dY), on every DMA tile with 16- and 4-byte
+    lanes, whole and split along the contraction (one sum per run, the runs
+    added in order), overwriting and accumulating; (520, 392, 264) has a K
+    tail in the product and ragged edge tiles."""
+    M, N, K = shape
+    inp = wl.linear(M, N, K, seed=31).make()
+    x, w, dy = (inp[k].to(DEV) for k in ("X", "W", "dY"))
+    prior = torch.randn(N, generator=torch.Generator().manual_seed(5)).to(DEV)
+    X, dY = to_f64(inp["X"]), to_f64(inp["dY"])
+    dW_ref, SW = oracle.linear_bwd_dw(dY, X)
+    db_ref, Sb = oracle.linear_bwd_db(dY)
+    for acc in (False, True):
+        dw = torch.zeros(N, K, device=DEV) if acc else torch.full((N, K), float("nan"), device=DEV)
+        db = prior.clone() if acc else torch.full((N,), float("nan"), device=DEV)
+        b.debug_set("cfg", cfg)
+        b.debug_set("vec1", vec1)
+        b.debug_set("splits", splits)
+        try:
+            need = b.linear_bwd_workspace(x, w, dy, None, dw, db)
+            need_dw = b.linear_bwd_workspace(x, w, dy, None, dw, None)
+            if splits:
+                # the runs' db sums sit after the partial tiles: the fold is in use
+                assert need == ((need_dw + 255) // 256) * 256 + splits * N * 4, (need, need_dw)
+            ws = torch.empty(need // 4 + 64, device=DEV) if need else None
+            b.linear_bwd(x, w, dy, None, dw, db, accumulate=acc, workspace=ws)
+            torch.cuda.synchronize()
+        finally:
+            b.debug_set("cfg", -1)
+            b.debug_set("vec1", 0)
+            b.debug_set("splits", 0)
+        base = prior.double().cpu().numpy() if acc else 0.0
+        assert_close(to_f64(db), db_ref + base, Sb + (1 if acc else 0), what=f"db (acc={acc})")
+        assert_close(to_f64(dw), dW_ref, SW, what="dW")
