@@ -35,6 +35,7 @@ EXPORTS = ["mt_linear_fwd", "mt_linear_bwd", "mt_linear_bwd_workspace", "mt_matm
            "mt_conv2d_fwd", "mt_conv2d_fwd_workspace", "mt_conv2d_bwd", "mt_conv2d_bwd_workspace",
            "mt_workspace_bytes", "mt_linear_bwd_noalloc"]
 NOALLOC_SCRATCH_BYTES = 32 << 20  # MT_NOALLOC_SCRATCH_BYTES
+NUM_GEMM_CFG = 16  # tile configurations mt_debug_set("cfg", i) accepts
 ACT = {"none": 0, "relu": 1, "sigmoid": 2, "tanh": 3, "gelu": 4}
 
 

@@ -116,12 +116,37 @@ int choose_cfg(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_spl
   const int c = choose_cfg_aligned(M, N, batch, stages, can_split, bf16, a_kc, b_kc, vec, K, red);
   if (vec || bf16 || c == mt::kCfg64x64) return c;
   if (cdiv(M, 256) * cdiv(N, 256) * batch >= 1024) return mt::kCfgDma256x256;
-  auto used = [&](int64_t bm, int64_t bn) {
-    return (double)(M * N) / (double)(cdiv(M, bm) * bm * cdiv(N, bn) * bn);
+  // Each candidate tile is scored by the share of its work that is useful:
+  // the output it covers inside the matrix, the K it covers inside the
+  // contraction, and how full its last round of blocks is (a product that
+  // will be split along K fills its round with the split). The tiles shaped
+  // for sizes just past a multiple of 128 (96- and 192-wide, 64-row) stand in
+  // for 128-wide tiles that would cover a third too much (measured on the
+  // 16x1x509x257 @ 1x8x257x383 products).
+  struct Cand {
+    int cfg, bm, bn, bk, per_cu;
   };
-  const double u8 = used(256, 128), u9 = used(128, 256), u10 = used(128, 128);
-  if (std::max(u8, u9) >= 0.9 * u10) return u8 >= u9 ? mt::kCfgDma256x128 : mt::kCfgDma128x256;
-  return mt::kCfgDma128x128;
+  const Cand cands[] = {{mt::kCfgDma256x128, 256, 128, 16, 2}, {mt::kCfgDma128x256, 128, 256, 16, 2},
+                        {mt::kCfgDma128x128, 128, 128, 32, 2}, {mt::kCfgDma256x192, 256, 192, 16, 1},
+                        {mt::kCfgDma256x96, 256, 96, 16, 2},   {mt::kCfgDma64x384, 64, 384, 16, 2}};
+  int best = mt::kCfgDma128x128;
+  double best_score = -1.0;
+  for (const Cand& t : cands) {
+    if (t.cfg == mt::kCfgDma256x96 && !b_kc) continue;  // its B tile must be K-contiguous
+    const int64_t blocks = cdiv(M, t.bm) * cdiv(N, t.bn) * batch;
+    const int64_t slots = 256 * t.per_cu;
+    const double used = (double)(M * N) / (double)(cdiv(M, t.bm) * t.bm * cdiv(N, t.bn) * t.bn);
+    const double kuse = K > 0 ? (double)K / (double)(cdiv(K, t.bk) * t.bk) : 1.0;
+    const bool split_fills = can_split && blocks < slots && stages >= 16;
+    const double fill = split_fills ? 1.0 : (double)blocks / (double)(cdiv(blocks, slots) * slots);
+    // the new tiles win only by a clear margin over the 128-multiple ones
+    const double score = used * kuse * fill * (t.cfg >= mt::kCfgDma256x192 ? 0.95 : 1.0);
+    if (score > best_score) {
+      best_score = score;
+      best = t.cfg;
+    }
+  }
+  return best;
 }
 
 int choose_cfg_aligned(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_split,
@@ -171,7 +196,7 @@ int choose_cfg_aligned(int64_t M, int64_t N, int64_t batch, int64_t stages, bool
 // run and at most 16 runs.
 int choose_splits(int64_t blocks, int64_t stages, int cfg) {
   if (g_force_splits > 0) return (int)std::min<int64_t>(g_force_splits, std::max<int64_t>(stages, 1));
-  if (cfg == mt::kCfgDma256x256 || cfg == mt::kCfgDma128x128k64) {
+  if (cfg == mt::kCfgDma256x256 || cfg == mt::kCfgDma128x128k64 || cfg == mt::kCfgDma256x192) {
     // one block per CU: runs that together fill the 256 CUs once, each at
     // least 1024 (256x256) or 512 (128x128 at BK = 64) deep in K
     if (blocks >= 256) return 1;
@@ -235,12 +260,15 @@ int vec_elems(bool bf16) { return bf16 ? 8 : 4; }
 
 // Whether the launcher runs tile configuration cfg on the DMA-ring kernel
 // (gemm_f32.hip / gemm_bf16.hip): bf16 only with 16-byte loads, fp32 with
-// 4-byte lanes on 256x256, 256x128, 128x256 and the 4-wave 128x128.
+// 4-byte lanes on 256x256, 256x128, 128x256, the 4-wave 128x128 and the
+// 256x192, 256x96 and 64x384 tiles.
 bool dma_kernel(int cfg, bool vec, bool bf16) {
   if (cfg < mt::kCfgDma256x256) return false;
   if (vec) return true;
   return !bf16 && (cfg == mt::kCfgDma256x256 || cfg == mt::kCfgDma256x128 ||
-                   cfg == mt::kCfgDma128x256 || cfg == mt::kCfgDma128x128);
+                   cfg == mt::kCfgDma128x256 || cfg == mt::kCfgDma128x128 ||
+                   cfg == mt::kCfgDma256x192 || cfg == mt::kCfgDma256x96 ||
+                   cfg == mt::kCfgDma64x384);
 }
 
 // Byte offset of the split runs' column sums of A in the workspace: after
@@ -262,13 +290,21 @@ size_t plan_gemm(GemmCall& g, bool may_split) {
   // the BK = 64 128x128 tile exists for fp32 with 16-byte lanes only
   if (g.cfg == mt::kCfgDma128x128k64 && (g.bf16 || !g.vec))
     g.cfg = g.bf16 ? mt::kCfgDma128x128 : mt::kCfgDma128x128w8;
+  // the 256x192, 256x96 and 64x384 tiles exist for fp32 with 4-byte lanes
+  // only, 256x96 with a K-contiguous B only
+  if ((g.cfg == mt::kCfgDma256x192 || g.cfg == mt::kCfgDma256x96 || g.cfg == mt::kCfgDma64x384) &&
+      (g.vec || g.bf16))
+    g.cfg = g.bf16 ? mt::kCfgDma128x128 : mt::kCfgDma256x128;
+  if (g.cfg == mt::kCfgDma256x96 && !g.b_kc) g.cfg = mt::kCfgDma256x128;
   // operands or output without 16-byte aligned rows: fp32 keeps the DMA tiles
   // (4-byte lanes, element stores) and maps the register-staged tiles above
   // 128x128 to them; the element-load register-staged kernels stop at 128x128
   if (!g.vec) {
     if (g.cfg == mt::kCfgDma128x128w8) g.cfg = mt::kCfgDma128x128;  // 4-byte lanes: 4 waves
     const bool dma = g.cfg == mt::kCfgDma256x256 || g.cfg == mt::kCfgDma256x128 ||
-                     g.cfg == mt::kCfgDma128x256 || g.cfg == mt::kCfgDma128x128;
+                     g.cfg == mt::kCfgDma128x256 || g.cfg == mt::kCfgDma128x128 ||
+                     g.cfg == mt::kCfgDma256x192 || g.cfg == mt::kCfgDma256x96 ||
+                     g.cfg == mt::kCfgDma64x384;
     if (!g.bf16 && (dma || g.cfg == mt::kCfg256x128 || g.cfg == mt::kCfg128x256)) {
       if (g.cfg == mt::kCfg256x128) g.cfg = mt::kCfgDma256x128;
       if (g.cfg == mt::kCfg128x256) g.cfg = mt::kCfgDma128x256;

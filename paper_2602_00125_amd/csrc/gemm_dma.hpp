@@ -108,7 +108,8 @@ struct DmaTile {
   static constexpr int EPC = 16 / ES;                   // elements per 16-byte chunk
   static_assert(BYTES % 1024 == 0, "tile must be whole 1 KB blocks");
   static_assert(!KC || RB == 64 || RB == 128 || RB == 256, "K-contiguous rows of 64 to 256 bytes");
-  static_assert(KC || RB >= 256, "M/N-contiguous rows of at least 256 bytes");
+  static_assert(KC || RB % 256 == 0, "M/N-contiguous rows of whole 256-byte groups (the swizzle "
+                                     "moves chunks within them)");
 
   static __device__ __forceinline__ int swz(int r) {
     if constexpr (KC) {

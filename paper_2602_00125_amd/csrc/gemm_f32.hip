@@ -50,6 +50,12 @@ static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream
       case kCfgDma256x128: return launch_dma<A_KC, B_KC, 256, 128, 16, 2, 2, 3, 2, false, 4, false>(p, stream);
       case kCfgDma128x256: return launch_dma<A_KC, B_KC, 128, 256, 16, 2, 2, 3, 2, false, 4, false>(p, stream);
       case kCfgDma128x128: return launch_dma<A_KC, B_KC, 128, 128, 32, 2, 2, 2, 2, false, 4, false>(p, stream);
+      case kCfgDma256x192: return launch_dma<A_KC, B_KC, 256, 192, 16, 4, 2, 4, 2, false, 4, false>(p, stream);
+      case kCfgDma256x96:
+        // an N-contiguous B would need 384-byte LDS rows, which the swizzle cannot serve
+        if constexpr (B_KC) return launch_dma<A_KC, B_KC, 256, 96, 16, 4, 1, 3, 2, false, 4, false>(p, stream);
+        else return hipErrorInvalidValue;
+      case kCfgDma64x384: return launch_dma<A_KC, B_KC, 64, 384, 16, 1, 4, 2, 2, false, 4, false>(p, stream);
       case kCfg64x64: return launch_f32<A_KC, B_KC, 64, 64, 16, 2, 2, 1, 4>(p, stream);
       default: return launch_f32<A_KC, B_KC, 128, 128, 16, 2, 2, 1, 2>(p, stream);
     }
@@ -75,7 +81,7 @@ static hipError_t launch_layout(const GemmParams& p, int cfg, hipStream_t stream
 int gemm_tile_m(int cfg) {
   switch (cfg) {
     case kCfg256x256: case kCfg256x128: case kCfg256x256x64w8: case kCfgDma256x256:
-    case kCfgDma256x256w4: case kCfgDma256x128: return 256;
+    case kCfgDma256x256w4: case kCfgDma256x128: case kCfgDma256x192: case kCfgDma256x96: return 256;
     case kCfg128x256: case kCfg128x128: case kCfgDma128x256: case kCfgDma128x128:
     case kCfgDma128x128w8: case kCfgDma128x128k64: return 128;
     default: return 64;
@@ -87,6 +93,9 @@ int gemm_tile_n(int cfg) {
     case kCfgDma256x256w4: case kCfgDma128x256: return 256;
     case kCfg256x128: case kCfg128x128: case kCfgDma256x128: case kCfgDma128x128:
     case kCfgDma128x128w8: case kCfgDma128x128k64: return 128;
+    case kCfgDma256x192: return 192;
+    case kCfgDma256x96: return 96;
+    case kCfgDma64x384: return 384;
     default: return 64;
   }
 }

@@ -26,7 +26,12 @@ enum GemmCfg {
   kCfgDma128x128 = 10,   // 128x128, 4 waves, BK = 32 / 64, 2-stage ring (64 KB), 2 blocks per CU
   kCfgDma128x128w8 = 11, // the same tile with 8 waves (fp32: 64x32 each; bf16: 32x64)
   kCfgDma128x128k64 = 12, // fp32 only: 128x128, 8 waves of 64x32, BK = 64, 2-stage ring (128 KB), 1 block per CU
-  kNumGemmCfg = 13
+  // fp32 operands without 16-byte aligned rows (4-byte lanes), tiles shaped
+  // for dimensions just past a multiple of 128 or 256 (every wave 64x96):
+  kCfgDma256x192 = 13,   // 8 waves, BK = 16, 4-stage ring (112 KB), 1 block per CU
+  kCfgDma256x96 = 14,    // 4 waves, BK = 16, 3-stage ring (66 KB), 2 blocks per CU; B K-contiguous
+  kCfgDma64x384 = 15,    // 4 waves, BK = 16, 2-stage ring (56 KB), 2 blocks per CU
+  kNumGemmCfg = 16
 };
 int gemm_tile_m(int cfg);
 int gemm_tile_n(int cfg);

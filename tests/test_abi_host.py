@@ -189,10 +189,10 @@ def test_workspace_queries_are_host_only():
 
 def test_debug_knobs_validate():
     assert b.lib.mt_debug_set(b"nope", 0) == -1
-    for key, bad in (("cfg", -2), ("cfg", 13), ("vec1", 2), ("splits", -1), ("parts", 5000),
+    for key, bad in (("cfg", -2), ("cfg", b.NUM_GEMM_CFG), ("vec1", 2), ("splits", -1), ("parts", 5000),
                      ("conv_gather", 2), ("stream_k", 3), ("sk_blocks", -1), ("phase_grid", 3)):
         assert b.lib.mt_debug_set(key.encode(), bad) == -2, (key, bad)
-    for key, ok in (("cfg", 12), ("cfg", -1), ("vec1", 1), ("vec1", 0), ("splits", 7), ("splits", 0),
+    for key, ok in (("cfg", b.NUM_GEMM_CFG - 1), ("cfg", -1), ("vec1", 1), ("vec1", 0), ("splits", 7), ("splits", 0),
                     ("parts", 3), ("parts", 0), ("stream_k", 1), ("sk_blocks", 0), ("conv_gather", 1)):
         assert b.lib.mt_debug_set(key.encode(), ok) == 0, (key, ok)
 
@@ -262,3 +262,23 @@ def test_planner_split_decisions():
     assert n.value == 4 * 1024 * 1024 * 4 + 4 * 1024 * 4
     assert need(8192, 8192, 8192, "dx") == 0 and need(8192, 8192, 8192, "dw") == 0
     assert need(256, 1024, 4096, "dx") == 4 * 256 * 4096 * 4
+
+
+def test_planner_broadcast_batch_tiles():
+    """The odd-pitch tiles chosen for the 16x1x509x257 @ 1x8x257x383 products,
+    seen through the workspace queries (host only): dA (509 x 257 outputs)
+    covers its 257 columns with three 96-wide tiles, 2 x 3 x 16 = 96 tiles
+    split five ways; dB (257 x 383 outputs) covers its 257 rows with five
+    64-row tiles of 384 columns, 40 tiles split twelve ways; the forward
+    (512 tiles of 256 x 192, two full rounds) needs no split."""
+    G = 1 << 36
+    n = ctypes.c_size_t(0)
+    A, B, C = D([16, 1, 509, 257], ptr=G), D([1, 8, 257, 383], ptr=2 * G), D([16, 8, 509, 383], ptr=3 * G)
+    dA, dB = D([16, 1, 509, 257], ptr=4 * G), D([1, 8, 257, 383], ptr=5 * G)
+    Bt = D([1, 8, 383, 257], ptr=2 * G, stride=[8 * 257 * 383, 257 * 383, 1, 383])
+    At = D([16, 1, 257, 509], ptr=G, stride=[509 * 257, 509 * 257, 1, 257])
+    assert b.lib.mt_matmul_workspace(R(A), R(B), R(C), 0, ctypes.byref(n)) == 0 and n.value == 0
+    assert b.lib.mt_matmul_workspace(R(C), R(Bt), R(dA), b.REDUCE_INTO, ctypes.byref(n)) == 0
+    assert n.value == 5 * 16 * 509 * 257 * 4
+    assert b.lib.mt_matmul_workspace(R(At), R(C), R(dB), b.REDUCE_INTO, ctypes.byref(n)) == 0
+    assert n.value == 12 * 8 * 257 * 383 * 4

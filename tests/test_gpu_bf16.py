@@ -69,7 +69,7 @@ def test_bf16_linear_small_and_ragged(M, N, K):
     check_full(inp, run(inp))
 
 
-@pytest.mark.parametrize("cfg", list(range(13)))
+@pytest.mark.parametrize("cfg", list(range(b.NUM_GEMM_CFG)))
 @pytest.mark.parametrize("vec1", [0, 1])
 @pytest.mark.parametrize("shape", [(520, 392, 264), (576, 320, 256)])
 def test_bf16_every_tile_config(cfg, vec1, shape):
