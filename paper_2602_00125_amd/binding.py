@@ -14,7 +14,9 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libminitensor_hip.so")
+# MT_LIB_OVERRIDE: a differently built copy of the library (the host-only
+# sanitizer build the CPU tests load); default: the in-tree build
+LIB_PATH = os.environ.get("MT_LIB_OVERRIDE") or os.path.join(_HERE, "libminitensor_hip.so")
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run `python paper_2602_00125_amd/build.py`")
 lib = ctypes.CDLL(LIB_PATH)

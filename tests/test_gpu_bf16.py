@@ -104,6 +104,14 @@ def test_bf16_linear_16384x8192x8192_sampled():
     check_bf16(to_f64(out["db"]), db, Sb, "db")
     for k in out:
         assert torch.isfinite(out[k]).all(), k
+    # whole 256-row bands at full contraction length, crossing a tile boundary
+    R, r0, n0 = 256, 8064, 2944
+    Yb, SY = oracle.linear_fwd(X[r0:r0 + R], W, B)
+    check_bf16(to_f64(out["Y"][r0:r0 + R]), Yb, SY, "Y (band)")
+    dXb, SX = oracle.linear_bwd_dx(dY[r0:r0 + R], W)
+    check_bf16(to_f64(out["dX"][r0:r0 + R]), dXb, SX, "dX (band)")
+    dWb, SW = oracle.linear_bwd_dw(np.ascontiguousarray(dY[:, n0:n0 + R]), X)
+    check_bf16(to_f64(out["dW"][n0:n0 + R]), dWb, SW, "dW (band)")
 
 
 def test_bf16_integer_inputs_bit_exact_at_16384x8192x8192():

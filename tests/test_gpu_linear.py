@@ -132,10 +132,26 @@ def _sampled_check(inp, out, n_random=3000):
         assert torch.isfinite(out[k]).all(), f"{k}: unwritten (NaN) or non-finite elements"
 
 
+def _band_check(inp, out, r0, n0, R=256):
+    """Whole 256-row bands at full contraction length against the row-major
+    oracle: rows r0..r0+R-1 of Y and dX (X and dY rows of the band) and rows
+    n0..n0+R-1 of dW (dY columns of the band)."""
+    X, W, B, dY = (to_f64(inp[k]) for k in ("X", "W", "b", "dY"))
+    Y, SY = oracle.linear_fwd(X[r0:r0 + R], W, B)
+    assert_close(to_f64(out["Y"][r0:r0 + R]), Y, SY, what=f"Y rows {r0}..{r0 + R - 1}")
+    dX, SX = oracle.linear_bwd_dx(dY[r0:r0 + R], W)
+    assert_close(to_f64(out["dX"][r0:r0 + R]), dX, SX, what=f"dX rows {r0}..{r0 + R - 1}")
+    dW, SW = oracle.linear_bwd_dw(np.ascontiguousarray(dY[:, n0:n0 + R]), X)
+    assert_close(to_f64(out["dW"][n0:n0 + R]), dW, SW, what=f"dW rows {n0}..{n0 + R - 1}")
+
+
 def test_linear_8192_cubed_sampled():
     inp = wl.LINEAR_8192x8192x8192_F32.make()
     out = run_linear(inp)
     _sampled_check(inp, out)
+    # one whole band each, crossing a 256-row tile boundary (rows 3968..4223
+    # of Y and dX, rows 6016..6271 of dW)
+    _band_check(inp, out, r0=3968, n0=6016)
 
 
 def test_linear_8192_cubed_integer_inputs_bit_exact():
