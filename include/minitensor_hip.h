@@ -368,16 +368,22 @@ mt_status mt_broadcast_shape(int32_t na, const int64_t* a, int32_t nb, const int
 mt_status mt_matmul_shape(int32_t na, const int64_t* a, int32_t nb, const int64_t* b,
                           int32_t* nout, int64_t* out);
 
-/* Testing and tuning knobs (process-wide, not thread-safe; 0 = accepted,
- * -1 = unknown key, -2 = value out of range). Keys: "cfg" GEMM tile
+/* Testing and tuning knobs, for tests and measurements only: each setting
+ * is process-wide and applies to every later call from any thread (the
+ * values are atomics, so setting one while calls run is safe, but which of
+ * those calls see it is unspecified; a production caller leaves them at
+ * their defaults). Returns 0 = accepted, -1 = unknown key, -2 = value out of
+ * range. Keys: "cfg" GEMM tile
  * configuration (-1 = automatic; register-staged tiles 0 = 256x256,
  * 1 = 256x128, 2 = 128x256, 3 = 128x128, 4 = 64x64, 5 = 256x256 with 8 waves;
  * tiles streamed straight into an LDS ring 6 = 256x256 with 8 waves,
  * 7 = 256x256 with 4 waves, 8 = 256x128, 9 = 128x256, 10 = 128x128,
  * 11 = 128x128 with 8 waves, 12 = 128x128 with 8 waves and 64-deep fp32
- * K-stages (bf16 maps it to 10); fp32 operands that do not allow 16-byte loads
- * run on tiles 6, 8, 9, 10 with 4-byte lanes (11 and 12 map to 10), else at
- * 128x128 or 64x64; bf16 ones at 128x128 or 64x64); "vec1"
+ * K-stages (bf16 maps it to 10), 13 = 256x192, 14 = 256x96 (K-contiguous B
+ * only, else 8), 15 = 64x384 (13-15: fp32 operands without 16-byte aligned
+ * rows only, else 8; bf16 10); fp32 operands that do not allow 16-byte loads
+ * run on tiles 6, 8, 9, 10 and 13-15 with 4-byte lanes (11 and 12 map to 10),
+ * else at 128x128 or 64x64; bf16 ones at 128x128 or 64x64); "vec1"
  * (1 = force the narrow-load kernels); "splits" (0..4096, split-K count for
  * mt_linear_bwd's dw, 0 = automatic); "parts" (0..4096, row slices of the db
  * and broadcast-gradient reductions, 0 = automatic); "krot" (1 = the default:

@@ -23,15 +23,15 @@ namespace mt::host {
 thread_local std::string g_err;
 
 // Knobs for tests and tuning (mt_debug_set): -1 / 0 = automatic.
-int g_force_cfg = -1;
-int g_force_vec1 = 0;
-int g_force_splits = 0;
-int g_force_parts = 0;
-int g_krot = 1;  // K-stage rotation per XCD in the DMA kernel (measured: bf16 NT +2%, others neutral)
-int g_conv_gather = 1;  // convolution products gather the image where the layout allows
-int g_stream_k = 1;     // gathered 256x256 convolution products: 0 never, 1 on a ragged last wave, 2 always
-int g_sk_blocks = 0;    // stream-K blocks (0: one per CU, 256)
-int g_phase_grid = 1;   // strided input gradient: 0 a launch per phase, 1 one grid when large, 2 always
+std::atomic<int> g_force_cfg{-1};
+std::atomic<int> g_force_vec1{0};
+std::atomic<int> g_force_splits{0};
+std::atomic<int> g_force_parts{0};
+std::atomic<int> g_krot{1};  // K-stage rotation per XCD in the DMA kernel (measured: bf16 NT +2%, others neutral)
+std::atomic<int> g_conv_gather{1};  // convolution products gather the image where the layout allows
+std::atomic<int> g_stream_k{1};     // gathered 256x256 convolution products: 0 never, 1 on a ragged last wave, 2 always
+std::atomic<int> g_sk_blocks{0};    // stream-K blocks (0: one per CU, 256)
+std::atomic<int> g_phase_grid{1};   // strided input gradient: 0 a launch per phase, 1 one grid when large, 2 always
 
 mt_status fail(mt_status s, const std::string& msg) {
   g_err = msg;
@@ -112,7 +112,7 @@ int choose_cfg_aligned(int64_t M, int64_t N, int64_t batch, int64_t stages, bool
 // outputs, 128x128 for 257 x 383).
 int choose_cfg(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_split, bool bf16,
                bool a_kc, bool b_kc, bool vec, int64_t K, int64_t red) {
-  if (g_force_cfg >= 0) return g_force_cfg;
+  if (const int fc = g_force_cfg; fc >= 0) return fc;
   const int c = choose_cfg_aligned(M, N, batch, stages, can_split, bf16, a_kc, b_kc, vec, K, red);
   if (vec || bf16 || c == mt::kCfg64x64) return c;
   if (cdiv(M, 256) * cdiv(N, 256) * batch >= 1024) return mt::kCfgDma256x256;
@@ -195,7 +195,7 @@ int choose_cfg_aligned(int64_t M, int64_t N, int64_t batch, int64_t stages, bool
 // two blocks per CU, aim for ~512 blocks in all, with at least 8 stages per
 // run and at most 16 runs.
 int choose_splits(int64_t blocks, int64_t stages, int cfg) {
-  if (g_force_splits > 0) return (int)std::min<int64_t>(g_force_splits, std::max<int64_t>(stages, 1));
+  if (const int fs = g_force_splits; fs > 0) return (int)std::min<int64_t>(fs, std::max<int64_t>(stages, 1));
   if (cfg == mt::kCfgDma256x256 || cfg == mt::kCfgDma128x128k64 || cfg == mt::kCfgDma256x192) {
     // one block per CU: runs that together fill the 256 CUs once, each at
     // least 1024 (256x256) or 512 (128x128 at BK = 64) deep in K
@@ -223,10 +223,9 @@ int choose_splits(int64_t blocks, int64_t stages, int cfg) {
 // nearest of them).
 int choose_epi_cfg(int64_t M, int64_t N, bool vec) {
   auto tiles = [&](int64_t bm, int64_t bn) { return cdiv(M, bm) * cdiv(N, bn); };
-  if (g_force_cfg >= 0) {
-    if ((g_force_cfg == mt::kCfgDma256x256 || g_force_cfg == mt::kCfgDma128x128) && vec)
-      return g_force_cfg;
-    if (g_force_cfg == mt::kCfg64x64) return g_force_cfg;
+  if (const int fc = g_force_cfg; fc >= 0) {
+    if ((fc == mt::kCfgDma256x256 || fc == mt::kCfgDma128x128) && vec) return fc;
+    if (fc == mt::kCfg64x64) return fc;
     return mt::kCfg128x128;
   }
   if (vec && tiles(256, 256) >= 256) return mt::kCfgDma256x256;
@@ -328,8 +327,10 @@ size_t plan_gemm(GemmCall& g, bool may_split) {
   // block per CU) whose tiles leave CUs idle: stream-K, every CU taking an
   // equal share of the tile-major K-stages; cut tiles are summed by a finish
   // pass
-  if ((g.conv == 1 || g.conv == 3) && g.cfg == mt::kCfgDma256x256 && g_stream_k) {
-    const int64_t G = g_sk_blocks > 0 ? g_sk_blocks : 256;
+  const int stream_k = g_stream_k;
+  if ((g.conv == 1 || g.conv == 3) && g.cfg == mt::kCfgDma256x256 && stream_k) {
+    const int sk_blocks = g_sk_blocks;
+    const int64_t G = sk_blocks > 0 ? sk_blocks : 256;
     const int64_t T = cdiv(p.M, 256) * cdiv(p.N, 256);
     // more tiles than CUs with a last wave under 90% full, or fewer tiles
     // than CUs (a split by whole runs leaves CUs idle) with at least 16
@@ -338,7 +339,7 @@ size_t plan_gemm(GemmCall& g, bool may_split) {
                          T * stages >= G * kDmaMinRunStages) ||
                         (T < G && T * stages >= G * 16);
     // (at least one stage per block keeps the block boundaries distinct)
-    if ((g_stream_k == 2 && T * stages >= G) || ragged) {
+    if ((stream_k == 2 && T * stages >= G) || ragged) {
       g.sk = (int)G;
       p.partial_stride = p.M * p.N;
       return (size_t)mt::sk_max_segments(T, stages, G) * p.M * p.N * sizeof(float);
@@ -537,7 +538,8 @@ mt_status linear_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tenso
   }
   int parts = 1;
   if (db && N > 0) {
-    parts = g_force_parts > 0 ? g_force_parts : mt::colsum_parts(M, N);
+    const int fp = g_force_parts;
+    parts = fp > 0 ? fp : mt::colsum_parts(M, N);
     if (parts > 1 && !fold_db) need_db = (size_t)parts * N * sizeof(float);
   }
   if (ws_query) {
@@ -679,7 +681,8 @@ mt_status reduce_impl(const mt_tensor* go, const mt_tensor* gi, uint32_t flags, 
   std::string err;
   if ((s = mt::plan_reduce(go->ndim, go->shape, go->stride, gi->ndim, gi->shape, &plan, &err)))
     return fail(s, "mt_reduce_broadcast_grad: " + err);
-  const int parts = g_force_parts > 0 ? g_force_parts : mt::reduce_parts(plan);
+  const int fp = g_force_parts;
+  const int parts = fp > 0 ? fp : mt::reduce_parts(plan);
   const size_t need = parts > 1 ? (size_t)parts * plan.keep_count * sizeof(float) : 0;
   if (ws_query) {
     *ws_query = need;
@@ -770,7 +773,7 @@ mt_status act_bwd_impl(int32_t act, const mt_tensor* z, const mt_tensor* dy, con
       overlaps(db, dz))
     return fail(MT_ERR_ALIAS, "an output overlaps an input or the other output");
   int parts = 1;
-  if (db && M > 0 && N > 0) parts = g_force_parts > 0 ? g_force_parts : mt::colsum_parts(M, N);
+  if (const int fp = g_force_parts; db && M > 0 && N > 0) parts = fp > 0 ? fp : mt::colsum_parts(M, N);
   const size_t need = parts > 1 ? (size_t)parts * N * sizeof(float) : 0;
   if (ws_query) {
     *ws_query = need;

@@ -359,7 +359,8 @@ mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
   int parts = 1;
   size_t need_db = 0;
   if (db && cp.M > 0) {
-    parts = g_force_parts > 0 ? g_force_parts : mt::colsum_parts(cp.M, g.CO);
+    const int fp = g_force_parts;
+    parts = fp > 0 ? fp : mt::colsum_parts(cp.M, g.CO);
     if (parts > 1) need_db = (size_t)parts * g.CO * sizeof(float);
   }
   // dx = V W in one product where dy can be gathered (V: dy over the
@@ -449,8 +450,8 @@ mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
     // 32 x 256 x 56 x 56, 3x3, stride 2: dx 0.308 ms against 0.355 for a launch
     // per phase; with 128 channels half of every tile would idle: 0.28 against 0.20)
     const double used = (double)g.C / (double)(cdiv(g.C, 256) * 256);
-    const bool one_grid =
-        g_phase_grid == 2 || (g_phase_grid == 1 && rows >= 256 * 64 && used >= 0.9);
+    const int pg = g_phase_grid;
+    const bool one_grid = pg == 2 || (pg == 1 && rows >= 256 * 64 && used >= 0.9);
     if (one_grid && !phases.empty() && (int)phases.size() <= mt::kMaxConvPhases && g.C % 4 == 0) {
       // one grid of 256x256 tiles: every phase's tiles run side by side
       mt::ConvPhases tab;
