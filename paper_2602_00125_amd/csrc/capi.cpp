@@ -156,7 +156,12 @@ int choose_cfg_aligned(int64_t M, int64_t N, int64_t batch, int64_t stages, bool
   // three layouts): the 256x256 tile whose operands stream straight into a
   // two-stage LDS ring, one block of 8 waves per CU, once there are enough
   // tiles to fill every CU.
-  if (tiles(256, 256) >= 256) return mt::kCfgDma256x256;
+  // bf16 with both operands K-contiguous (the forward layout) takes the
+  // 4-wave form, 128x128 accumulators per wave (measured on 16384 x 8192 x
+  // 8192: NT 1.889 -> 1.810 ms; NN 1.809 -> 1.828 and TN 1.788 -> 1.858 ms,
+  // so those keep 8 waves)
+  if (tiles(256, 256) >= 256)
+    return bf16 && a_kc && b_kc ? mt::kCfgDma256x256w4 : mt::kCfgDma256x256;
   // A few such tiles over a long contraction (e.g. the weight gradient of a
   // convolution, K = every output pixel): the same tile, its K-stages split
   // into runs that fill the chip once, each run at least kDmaMinRunStages long
@@ -166,9 +171,6 @@ int choose_cfg_aligned(int64_t M, int64_t N, int64_t batch, int64_t stages, bool
     if (t > 0 && 256 / t >= 2 && dma_stages / (256 / t) >= kDmaMinRunStages)
       return mt::kCfgDma256x256;
   }
-  (void)a_kc;
-  (void)b_kc;
-  (void)bf16;
   if (tiles(128, 256) >= 512) return N >= M ? mt::kCfg128x256 : mt::kCfg256x128;
   // mid-size products: the 128x128 tile streamed into an LDS ring, two blocks
   // per CU (measured on 4096 x 1024 x 1024: 96-106 TFLOP/s fp32 against 88-93
