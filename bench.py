@@ -68,6 +68,9 @@ def parse():
                          "per step instead of one per kernel; for launch-bound sizes)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target wall time of the CPU-oracle baseline sample (0 disables it)")
+    ap.add_argument("--torch-reference", action="store_true",
+                    help="linear workloads: also time torch's own products on the same device inputs "
+                         "(context only; never part of value)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (calibrates HBM "
                          "byte counters against a kernel of known traffic) and exit")
@@ -137,6 +140,38 @@ def cpu_baseline(inp, seconds: float):
                       f"and of dX = dY W and {R} full rows of dW = dY^T X (the oracle's row-major "
                       f"fp64 functions with the |a*b| bound, full contraction length) in {el:.1f} s; "
                       f"TFLOP/s = 2*MACs/s"}
+
+
+def torch_reference(x, w, b, dy, steps: int):
+    """torch's own products of the same layer on the same device inputs (the
+    library it calls, for context): Y = X W^T + b, dX = dY W, dW = dY^T X,
+    db = 1^T dY, each timed with events after a second of warm-up. bf16
+    products return bf16 there (fp32 here)."""
+    import torch
+
+    ops = {"fwd": lambda: torch.addmm(b.to(x.dtype), x, w.t()),
+           "dx": lambda: dy @ w,
+           "dw": lambda: dy.t() @ x,
+           "db": lambda: dy.sum(0, dtype=torch.float32)}
+    M, K = x.shape
+    N = w.shape[0]
+    out = {}
+    for name, fn in ops.items():
+        t = time.perf_counter()
+        while time.perf_counter() - t < 1.0:
+            fn()
+            torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        out[name] = {"ms": round(ms, 4)}
+        if name != "db":
+            out[name]["tflops"] = round(2.0 * M * N * K / (ms * 1e-3) / 1e12, 1)
+    return out
 
 
 WARMUP_USED = [None]  # warm-up steps of the run's timed pass (reported as "warmup")
@@ -569,6 +604,8 @@ def main():
         "colsum_alone": {"ms": round(cs_list[0], 4),
                          "gbs": round(db_bytes / (cs_list[0] * 1e-3) / 1e9, 1), "bytes": db_bytes},
     }
+    if args.torch_reference:
+        out["torch_reference"] = torch_reference(x, wt, bias, dy, args.steps)
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
     else:
