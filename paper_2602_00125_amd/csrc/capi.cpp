@@ -31,6 +31,7 @@ std::atomic<int> g_krot{1};  // K-stage rotation per XCD in the DMA kernel (meas
 std::atomic<int> g_conv_gather{1};  // convolution products gather the image where the layout allows
 std::atomic<int> g_stream_k{1};     // gathered 256x256 convolution products: 0 never, 1 on a ragged last wave, 2 always
 std::atomic<int> g_sk_blocks{0};    // stream-K blocks (0: one per CU, 256)
+std::atomic<int> g_persist{1};      // plain bf16 products on the 256x256 DMA tiles: one block per CU walking its tiles
 std::atomic<int> g_phase_grid{1};   // strided input gradient: 0 a launch per phase, 1 one grid when large, 2 always
 
 mt_status fail(mt_status s, const std::string& msg) {
@@ -235,6 +236,14 @@ int choose_epi_cfg(int64_t M, int64_t N, bool vec) {
   return mt::kCfg64x64;
 }
 
+// compute units of the current device (0 if the query fails)
+int cu_count() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  return cus;
+}
+
 void init_params(mt::GemmParams* p) {
   std::memset(p, 0, sizeof(*p));
   p->keep_count = 1;
@@ -387,6 +396,18 @@ mt_status launch_gemm(GemmCall& g, hipStream_t stream, void* ws, size_t ws_bytes
   if (rows_a * p.lda * es >= (int64_t)1 << 31 || rows_b * p.ldb * es >= (int64_t)1 << 31)
     return fail(MT_ERR_LAYOUT, "row pitch too large for 32-bit tile offsets");
   (void)hipGetLastError();  // clear a stale error so the launch check is ours
+  // plain bf16 products on the one-block-per-CU DMA tiles with more tiles
+  // than CUs and whole tiles only (M, N multiples of 256): a persistent grid, whose blocks run their tiles back to back so
+  // that each tile's first loads overlap the previous tile's last stage and
+  // its stores overlap the next tile's work
+  p.persist = 0;
+  if (g_persist && g.bf16 && !g.conv && !g.sk && g.vec && p.splits == 1 && p.keep_count == 1 &&
+      p.red_count == 1 && !p.colsum && !p.z && p.act == 0 && !p.accumulate &&
+      (g.cfg == mt::kCfgDma256x256 || g.cfg == mt::kCfgDma256x256w4)) {
+    const int cus = cu_count() & ~7;
+    if (cus >= 8 && p.M % 256 == 0 && p.N % 256 == 0 && (p.M / 256) * (p.N / 256) > cus)
+      p.persist = cus;
+  }
   if (g.sk) return hip_status(mt::gemm_f32_conv_sk(p, g.conv, g.sk, stream));
   hipError_t e = g.conv   ? mt::gemm_f32_conv(p, g.conv, g.cfg, stream)
                  : g.bf16 ? mt::gemm_bf16(p, g.a_kc, g.b_kc, g.vec, g.cfg, stream)
@@ -1232,6 +1253,9 @@ int mt_debug_set(const char* key, int64_t value) {
   } else if (!std::strcmp(key, "stream_k")) {
     if (value < 0 || value > 2) return -2;
     g_stream_k = (int)value;
+  } else if (!std::strcmp(key, "persist")) {
+    if (value < 0 || value > 1) return -2;
+    g_persist = (int)value;
   } else if (!std::strcmp(key, "phase_grid")) {
     if (value < 0 || value > 2) return -2;
     g_phase_grid = (int)value;

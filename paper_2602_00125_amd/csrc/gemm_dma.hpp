@@ -501,9 +501,12 @@ struct DmaMma<__bf16, A_KC, B_KC, TM, TN, BK, BM, BN> {
   }
 };
 
+// PERSIST: the grid holds one block per CU and block b computes the tiles
+// the plain grid's blocks b, b + gridDim.x, ... would (plain products only).
 template <typename T, bool A_KC, bool B_KC, int BM, int BN, int BK, int WGM, int WGN, int NS,
           int DMA_G0, int DMA_GS, bool KTAIL,
-          int WAVES_PER_EU, bool EPI = false, int DMA_LANE = 16, bool VEC_C = true>
+          int WAVES_PER_EU, bool EPI = false, int DMA_LANE = 16, bool VEC_C = true,
+          bool PERSIST = false>
 __global__ __launch_bounds__(WGM * WGN * 64)
 __attribute__((amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
 void gemm_dma_kernel(const GemmParams p) {
@@ -529,6 +532,7 @@ void conv_dma_kernel(const GemmParams p) {
   constexpr bool SK = false, sk_part = false;
   constexpr int64_t sk_t = 0, sk_ka = 0, sk_kb = 0;
   constexpr int sk_slot = 0;
+  constexpr bool PERSIST = false;
 #include "gemm_dma_body.inc"
 }
 
@@ -576,6 +580,7 @@ void conv_dma_sk_kernel(const GemmParams p) {
     const SkSeg seg = sk_segment(sk_t, sk_ka, ks_all, G, U);
     const bool sk_part = seg.n > 1;
     const int sk_slot = seg.slot;
+  constexpr bool PERSIST = false;
 #include "gemm_dma_body.inc"
     u = sk_t * ks_all + sk_kb;
     __syncthreads();  // the next segment's loads reuse the ring
@@ -617,6 +622,7 @@ void conv_dgrad_phases_kernel(const GemmParams p0, const ConvPhases tab) {
   p.cg.ho_shift = f.ho_shift;
   const int64_t sk_t = (int64_t)blockIdx.x - tab.tile0[k];
   const int64_t sk_ka = 0, sk_kb = (f.K + BK - 1) / BK;
+  constexpr bool PERSIST = false;
 #include "gemm_dma_body.inc"
 }
 

@@ -104,6 +104,11 @@ struct GemmParams {
   // colsum_part[s * M + m] and the host adds the runs in order. Null: off.
   float* colsum;
   float* colsum_part;
+  // DMA kernels, plain products of whole 256x256 tiles (no batch, split,
+  // column sums, activation or accumulation, M and N multiples of 256):
+  // the size of a persistent grid (one block per CU, each walking the tiles
+  // of the plain grid's blocks b, b + persist, ...); 0: the plain grid
+  int32_t persist;
 };
 
 }  // namespace mt

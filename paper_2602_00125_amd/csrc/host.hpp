@@ -15,7 +15,7 @@ namespace mt::host {
 
 // knobs set by mt_debug_set (-1 / 0 = automatic); atomics, read once per use
 extern std::atomic<int> g_force_cfg, g_force_vec1, g_force_splits, g_force_parts, g_krot;
-extern std::atomic<int> g_conv_gather, g_stream_k, g_sk_blocks, g_phase_grid;
+extern std::atomic<int> g_conv_gather, g_stream_k, g_sk_blocks, g_phase_grid, g_persist;
 
 // records the message for mt_last_error() and returns s
 mt_status fail(mt_status s, const std::string& msg);

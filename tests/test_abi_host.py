@@ -190,10 +190,12 @@ def test_workspace_queries_are_host_only():
 def test_debug_knobs_validate():
     assert b.lib.mt_debug_set(b"nope", 0) == -1
     for key, bad in (("cfg", -2), ("cfg", b.NUM_GEMM_CFG), ("vec1", 2), ("splits", -1), ("parts", 5000),
-                     ("conv_gather", 2), ("stream_k", 3), ("sk_blocks", -1), ("phase_grid", 3)):
+                     ("conv_gather", 2), ("stream_k", 3), ("sk_blocks", -1), ("phase_grid", 3),
+                     ("persist", 2), ("persist", -1)):
         assert b.lib.mt_debug_set(key.encode(), bad) == -2, (key, bad)
     for key, ok in (("cfg", b.NUM_GEMM_CFG - 1), ("cfg", -1), ("vec1", 1), ("vec1", 0), ("splits", 7), ("splits", 0),
-                    ("parts", 3), ("parts", 0), ("stream_k", 1), ("sk_blocks", 0), ("conv_gather", 1)):
+                    ("parts", 3), ("parts", 0), ("stream_k", 1), ("sk_blocks", 0), ("conv_gather", 1),
+                    ("persist", 0), ("persist", 1)):
         assert b.lib.mt_debug_set(key.encode(), ok) == 0, (key, ok)
 
 
