@@ -388,8 +388,18 @@ mt_status mt_matmul_shape(int32_t na, const int64_t* a, int32_t nb, const int64_
  * mt_linear_bwd's dw, 0 = automatic); "parts" (0..4096, row slices of the db
  * and broadcast-gradient reductions, 0 = automatic); "krot" (1 = the default:
  * blocks of the 256x256 DMA tile start their K loop at a stage that depends
- * on their XCD and wrap around; 0 = every block starts at k = 0). Results stay within the
- * documented accuracy for every setting. */
+ * on their XCD and wrap around; 0 = every block starts at k = 0); "persist"
+ * (1 = the default: plain bf16 products of whole 256x256 tiles, more tiles
+ * than CUs, no accumulate, run on a grid of one block per CU that walks the
+ * plain grid's tiles; 0 = the plain grid; the two give identical bits);
+ * convolution: "conv_gather" (1 = the default: products gather the image
+ * where the layout allows; 0 = always unfold), "stream_k" (gathered 256x256
+ * forward and input-gradient products: 0 never, 1 = the default: when the
+ * last round of blocks would be ragged, 2 always), "sk_blocks" (0..65535
+ * stream-K blocks, 0 = one per CU), "phase_grid" (strided input gradient:
+ * 0 a launch per sub-pixel phase, 1 = the default: one grid when large,
+ * 2 always one grid). Results stay within the documented accuracy for
+ * every setting. */
 int mt_debug_set(const char* key, int64_t value);
 
 /* Static description of a status code. */
