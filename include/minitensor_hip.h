@@ -389,7 +389,7 @@ mt_status mt_matmul_shape(int32_t na, const int64_t* a, int32_t nb, const int64_
  * and broadcast-gradient reductions, 0 = automatic); "krot" (1 = the default:
  * blocks of the 256x256 DMA tile start their K loop at a stage that depends
  * on their XCD and wrap around; 0 = every block starts at k = 0); "persist"
- * (1 = the default: plain bf16 products of whole 256x256 tiles, more tiles
+ * (1 = the default: plain products of whole 256x256 tiles, more tiles
  * than CUs, no accumulate, run on a grid of one block per CU that walks the
  * plain grid's tiles; 0 = the plain grid; the two give identical bits);
  * convolution: "conv_gather" (1 = the default: products gather the image

@@ -31,7 +31,7 @@ std::atomic<int> g_krot{1};  // K-stage rotation per XCD in the DMA kernel (meas
 std::atomic<int> g_conv_gather{1};  // convolution products gather the image where the layout allows
 std::atomic<int> g_stream_k{1};     // gathered 256x256 convolution products: 0 never, 1 on a ragged last wave, 2 always
 std::atomic<int> g_sk_blocks{0};    // stream-K blocks (0: one per CU, 256)
-std::atomic<int> g_persist{1};      // plain bf16 products on the 256x256 DMA tiles: one block per CU walking its tiles
+std::atomic<int> g_persist{1};      // plain products on the 256x256 DMA tiles: one block per CU walking its tiles
 std::atomic<int> g_phase_grid{1};   // strided input gradient: 0 a launch per phase, 1 one grid when large, 2 always
 
 mt_status fail(mt_status s, const std::string& msg) {
@@ -396,12 +396,12 @@ mt_status launch_gemm(GemmCall& g, hipStream_t stream, void* ws, size_t ws_bytes
   if (rows_a * p.lda * es >= (int64_t)1 << 31 || rows_b * p.ldb * es >= (int64_t)1 << 31)
     return fail(MT_ERR_LAYOUT, "row pitch too large for 32-bit tile offsets");
   (void)hipGetLastError();  // clear a stale error so the launch check is ours
-  // plain bf16 products on the one-block-per-CU DMA tiles with more tiles
+  // plain products on the one-block-per-CU DMA tiles with more tiles
   // than CUs and whole tiles only (M, N multiples of 256): a persistent grid, whose blocks run their tiles back to back so
   // that each tile's first loads overlap the previous tile's last stage and
   // its stores overlap the next tile's work
   p.persist = 0;
-  if (g_persist && g.bf16 && !g.conv && !g.sk && g.vec && p.splits == 1 && p.keep_count == 1 &&
+  if (g_persist && !g.conv && !g.sk && g.vec && p.splits == 1 && p.keep_count == 1 &&
       p.red_count == 1 && !p.colsum && !p.z && p.act == 0 && !p.accumulate &&
       (g.cfg == mt::kCfgDma256x256 || g.cfg == mt::kCfgDma256x256w4)) {
     const int cus = cu_count() & ~7;

@@ -29,6 +29,15 @@ static hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
   const int64_t blocks = (int64_t)q.tiles_m * q.tiles_n * p.keep_count * p.splits;
   if (blocks <= 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
+  // persistent grid (host decides: plain product of whole tiles, more tiles than CUs)
+  if constexpr (BM == 256 && BN == 256 && !EPI && LANE == 16 && VEC_C) {
+    if (p.persist > 0 && p.K % BK == 0 && blocks > p.persist) {
+      hipLaunchKernelGGL((gemm::gemm_dma_kernel<float, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 1, 1, false, WPE,
+                                                false, 16, true, true>),
+                         dim3((unsigned)p.persist), dim3(WGM * WGN * 64), 0, stream, q);
+      return hipGetLastError();
+    }
+  }
   // the per-load K-tail test only where K is not a whole number of stages
   if (p.K % BK != 0)
     hipLaunchKernelGGL((gemm::gemm_dma_kernel<float, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 1, 1, true, WPE, EPI, LANE, VEC_C>),

@@ -284,3 +284,71 @@ def test_linear_db_folded_into_dw(cfg, vec1, splits, shape):
         base = prior.double().cpu().numpy() if acc else 0.0
         assert_close(to_f64(db), db_ref + base, Sb + (1 if acc else 0), what=f"db (acc={acc})")
         assert_close(to_f64(dw), dW_ref, SW, what="dW")
+
+
+def _three_products(inp):
+    """Y, dX and dW as three calls (dW without db, so that no column sum
+    rides on it)."""
+    x, w, bias, dy = (inp[k].to(DEV) for k in ("X", "W", "b", "dY"))
+    M, K = x.shape
+    N = w.shape[0]
+    y = torch.full((M, N), float("nan"), device=DEV)
+    dx = torch.full((M, K), float("nan"), device=DEV)
+    dw = torch.full((N, K), float("nan"), device=DEV)
+    b.linear_fwd(x, w, bias, y)
+    b.linear_bwd(x, w, dy, dx, None, None)
+    b.linear_bwd(x, w, dy, None, dw, None)
+    torch.cuda.synchronize()
+    return {"Y": y, "dX": dx, "dW": dw}
+
+
+def _persist_on_off(inp):
+    try:
+        b.debug_set("persist", 1)
+        got = _three_products(inp)
+        b.debug_set("persist", 0)
+        plain = _three_products(inp)
+    finally:
+        b.debug_set("persist", 1)
+    return got, plain
+
+
+# (M, N, K) with 17 x 16 = 272 whole output tiles of 256x256 (more than the
+# CUs) for one product each: the forward (Y is M x N, with the bias), dX
+# (M x K) and dW (N x K); six K-stages of 32 in the product that is persistent
+PERSIST_SHAPES = {"Y": (4352, 4096, 192), "dX": (4352, 192, 4096), "dW": (192, 4352, 4096)}
+
+
+@pytest.mark.parametrize("cfg", [6, 7])
+@pytest.mark.parametrize("which", ["Y", "dX", "dW"])
+def test_persistent_grid(cfg, which):
+    """A product with more 256x256 tiles than CUs runs on a persistent grid
+    (one block per CU, the first 16 blocks taking two tiles): every element
+    against the oracle, and bit for bit against the plain grid, whose block
+    for each tile sums in the same order."""
+    M, N, K = PERSIST_SHAPES[which]
+    inp = wl.linear(M, N, K, seed=43).make()
+    b.debug_set("cfg", cfg)
+    try:
+        got, plain = _persist_on_off(inp)
+    finally:
+        b.debug_set("cfg", -1)
+    for k in ("Y", "dX", "dW"):
+        assert torch.equal(got[k], plain[k]), k
+    X, W, B, dY = (to_f64(inp[k]) for k in ("X", "W", "b", "dY"))
+    if which == "Y":
+        want, S = oracle.linear_fwd(X, W, B)
+    elif which == "dX":
+        want, S = oracle.linear_bwd_dx(dY, W)
+    else:
+        want, S = oracle.linear_bwd_dw(dY, X)
+    assert_close(to_f64(got[which]), want, S, what=which + " (persistent grid)")
+
+
+def test_persistent_grid_bitwise_at_8192_cubed():
+    """The bench's products on the persistent grid (1024 tiles, four per
+    block) equal the plain grid's bit for bit."""
+    got, plain = _persist_on_off(wl.LINEAR_8192x8192x8192_F32.make())
+    for k in ("Y", "dX", "dW"):
+        assert not torch.isnan(got[k]).any(), k
+        assert torch.equal(got[k], plain[k]), k
