@@ -197,6 +197,19 @@ def test_linear_accumulate():
     assert_close(to_f64(out["db"]), ref["db"][0] + prior["db"].double().numpy(), ref["db"][1] + 1, what="db+=")
 
 
+def test_linear_accumulate_on_whole_tiles():
+    """dX += dY W on a product with more whole 256x256 tiles than CUs (the
+    shape that runs on the persistent grid when it overwrites): the
+    accumulating product takes the plain grid and adds to the prior."""
+    M, N, K = 4352, 192, 4096
+    inp = wl.linear(M, N, K, seed=23).make()
+    prior = {"dx": torch.randn(M, K)}
+    out = run_linear(inp, accumulate=True, prior=prior, outputs=("dx",))
+    dY, W = to_f64(inp["dY"]), to_f64(inp["W"])
+    dX, SX = oracle.linear_bwd_dx(dY, W)
+    assert_close(to_f64(out["dX"]), dX + prior["dx"].double().numpy(), SX + 1, what="dX+= (whole tiles)")
+
+
 @pytest.mark.parametrize("outputs", [("dx",), ("dw",), ("db",), ("dx", "db"), ()])
 def test_linear_optional_outputs(outputs):
     inp = wl.linear(130, 70, 40, seed=3).make()
