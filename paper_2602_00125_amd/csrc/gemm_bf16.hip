@@ -33,7 +33,12 @@ static hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
   // persistent grid (host decides: plain product, more tiles than CUs)
   if constexpr (BM == 256 && BN == 256 && !EPI) {
     if (p.persist > 0 && p.K % BK == 0 && blocks > p.persist) {
-      hipLaunchKernelGGL((gemm::gemm_dma_kernel<__bf16, A_KC, B_KC, BM, BN, BK, WGM, WGN, NS, 1, 1, false, WPE,
+      // products with a K-contiguous A take the ring of five half-slots (the
+      // A and B tiles of a stage loaded in different halves of the stage
+      // before: forward +2%, dX +0.3% against the two-stage ring); the TN
+      // product keeps the two-stage ring (3% slower on the half-slots)
+      constexpr int NSP = A_KC ? 5 : NS;
+      hipLaunchKernelGGL((gemm::gemm_dma_kernel<__bf16, A_KC, B_KC, BM, BN, BK, WGM, WGN, NSP, 1, 1, false, WPE,
                                                 false, 16, true, true>),
                          dim3((unsigned)p.persist), dim3(WGM * WGN * 64), 0, stream, q);
       return hipGetLastError();
