@@ -153,6 +153,16 @@ int choose_cfg(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_spl
 int choose_cfg_aligned(int64_t M, int64_t N, int64_t batch, int64_t stages, bool can_split,
                        bool bf16, bool a_kc, bool b_kc, bool vec, int64_t K, int64_t red) {
   auto tiles = [&](int64_t bm, int64_t bn) { return cdiv(M, bm) * cdiv(N, bn) * batch; };
+  // share of a tile grid's output that lies inside the matrix
+  auto used = [&](int64_t bm, int64_t bn) {
+    return (double)(M * N) / (double)(cdiv(M, bm) * bm * cdiv(N, bn) * bn);
+  };
+  // fp32 products of fewer than ~4 waves of 256x256 tiles on which that tile
+  // computes far more than the matrix (e.g. 384 columns as 512) take the
+  // smaller tiles below instead (measured on 16 x 8 products of 509 x 384 x
+  // 260 and on the gradients of both operands summed over the broadcast axes:
+  // 135, 197 and 164 us against 175, 262 and 267 on 256x256)
+  const bool wide_waste = !bf16 && M > 0 && N > 0 && tiles(256, 256) < 1024 && used(256, 256) < 0.85;
   // Large products (measured on 8192^3 fp32 and 16384x8192x8192 bf16, all
   // three layouts): the 256x256 tile whose operands stream straight into a
   // two-stage LDS ring, one block of 8 waves per CU, once there are enough
@@ -161,12 +171,12 @@ int choose_cfg_aligned(int64_t M, int64_t N, int64_t batch, int64_t stages, bool
   // 4-wave form, 128x128 accumulators per wave (measured on 16384 x 8192 x
   // 8192: NT 1.889 -> 1.810 ms; NN 1.809 -> 1.828 and TN 1.788 -> 1.858 ms,
   // so those keep 8 waves)
-  if (tiles(256, 256) >= 256)
+  if (tiles(256, 256) >= 256 && !wide_waste)
     return bf16 && a_kc && b_kc ? mt::kCfgDma256x256w4 : mt::kCfgDma256x256;
   // A few such tiles over a long contraction (e.g. the weight gradient of a
   // convolution, K = every output pixel): the same tile, its K-stages split
   // into runs that fill the chip once, each run at least kDmaMinRunStages long
-  if (can_split && (vec || !bf16)) {
+  if (can_split && (vec || !bf16) && !wide_waste) {
     const int64_t t = tiles(256, 256);
     const int64_t dma_stages = cdiv(K, bf16 ? 64 : 32) * red;
     if (t > 0 && 256 / t >= 2 && dma_stages / (256 / t) >= kDmaMinRunStages)

@@ -140,6 +140,24 @@ def test_bmm_aligned_vector_path_and_accumulate():
     assert_close(to_f64(C), Cr + to_f64(prior), SC + 1, what="C+=")
 
 
+def test_bmm_aligned_rows_with_wide_edge_tiles():
+    """Aligned rows (pitches 260 and 384) on sizes where 256x256 tiles would
+    cover 384 columns as 512: the products take the smaller tiles; all three
+    against the oracle, the gradients summed over the broadcast axes."""
+    A = wl.tensor((4, 1, 509, 260), ("uniform", 1.0), seed=5)
+    B = wl.tensor((1, 8, 260, 384), ("uniform", 1.0), seed=6)
+    dC = wl.tensor((4, 8, 509, 384), ("normal",), seed=7)
+    Ad, Bd, dCd = A.to(DEV), B.to(DEV), dC.to(DEV)
+    C = gpu_matmul(Ad, (4, 8, 509, 384), Bd)
+    dA, dB = bmm_grads_folded(Ad, Bd, dCd)
+    An, Bn, dCn = A.double().numpy(), B.double().numpy(), dC.double().numpy()
+    Cr, SC = oracle.matmul(An, Bn)
+    assert_close(to_f64(C), Cr, SC, what="C")
+    dAr, SA, dBr, SB = oracle.matmul_bwd(An, Bn, dCn)
+    assert_close(to_f64(dA), dAr, SA, what="dA")
+    assert_close(to_f64(dB), dBr, SB, what="dB")
+
+
 def test_bmm_empty_and_zero_k():
     A = torch.randn(3, 4, 0, device=DEV)
     B = torch.randn(0, 5, device=DEV)
