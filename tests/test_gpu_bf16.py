@@ -212,12 +212,15 @@ def _persist_on_off(inp):
 # (M, N, K) with 17 x 16 = 272 whole output tiles of 256x256 (more than the
 # CUs) for one product each: the forward (Y is M x N, with the bias), dX
 # (M x K) and dW (N x K); three K-stages of 64 in the product that is
-# persistent
-PERSIST_SHAPES = {"Y": (4352, 4096, 192), "dX": (4352, 192, 4096), "dW": (192, 4352, 4096)}
+# persistent, or one (the forward and dX take the ring of half-slots, whose
+# A loads run a stage ahead of the B loads: with one stage per tile they
+# are a whole tile ahead)
+PERSIST_SHAPES = {"Y": (4352, 4096, 192), "dX": (4352, 192, 4096), "dW": (192, 4352, 4096),
+                  "Y1": (4352, 4096, 64), "dX1": (4352, 64, 4096)}
 
 
 @pytest.mark.parametrize("cfg", [6, 7])
-@pytest.mark.parametrize("which", ["Y", "dX", "dW"])
+@pytest.mark.parametrize("which", ["Y", "dX", "dW", "Y1", "dX1"])
 def test_bf16_persistent_grid(cfg, which):
     """A product with more 256x256 tiles than CUs runs on a persistent grid
     (one block per CU, the first 16 blocks taking two tiles): every element
@@ -233,13 +236,14 @@ def test_bf16_persistent_grid(cfg, which):
     for k in ("Y", "dX", "dW"):
         assert torch.equal(got[k], plain[k]), k
     X, W, B, dY = (to_f64(inp[k]) for k in ("X", "W", "b", "dY"))
-    if which == "Y":
+    out = which.rstrip("1")
+    if out == "Y":
         want, S = oracle.linear_fwd(X, W, B)
-    elif which == "dX":
+    elif out == "dX":
         want, S = oracle.linear_bwd_dx(dY, W)
     else:
         want, S = oracle.linear_bwd_dw(dY, X)
-    check_bf16(to_f64(got[which]), want, S, which + " (persistent grid)")
+    check_bf16(to_f64(got[out]), want, S, which + " (persistent grid)")
 
 
 def test_bf16_persistent_grid_bitwise_at_16384x8192x8192():

@@ -328,12 +328,14 @@ def _persist_on_off(inp):
 
 # (M, N, K) with 17 x 16 = 272 whole output tiles of 256x256 (more than the
 # CUs) for one product each: the forward (Y is M x N, with the bias), dX
-# (M x K) and dW (N x K); six K-stages of 32 in the product that is persistent
-PERSIST_SHAPES = {"Y": (4352, 4096, 192), "dX": (4352, 192, 4096), "dW": (192, 4352, 4096)}
+# (M x K) and dW (N x K); six K-stages of 32 in the product that is
+# persistent, or one (the loaders move to the next tile at every stage)
+PERSIST_SHAPES = {"Y": (4352, 4096, 192), "dX": (4352, 192, 4096), "dW": (192, 4352, 4096),
+                  "Y1": (4352, 4096, 32), "dX1": (4352, 32, 4096)}
 
 
 @pytest.mark.parametrize("cfg", [6, 7])
-@pytest.mark.parametrize("which", ["Y", "dX", "dW"])
+@pytest.mark.parametrize("which", ["Y", "dX", "dW", "Y1", "dX1"])
 def test_persistent_grid(cfg, which):
     """A product with more 256x256 tiles than CUs runs on a persistent grid
     (one block per CU, the first 16 blocks taking two tiles): every element
@@ -349,13 +351,14 @@ def test_persistent_grid(cfg, which):
     for k in ("Y", "dX", "dW"):
         assert torch.equal(got[k], plain[k]), k
     X, W, B, dY = (to_f64(inp[k]) for k in ("X", "W", "b", "dY"))
-    if which == "Y":
+    out = which.rstrip("1")
+    if out == "Y":
         want, S = oracle.linear_fwd(X, W, B)
-    elif which == "dX":
+    elif out == "dX":
         want, S = oracle.linear_bwd_dx(dY, W)
     else:
         want, S = oracle.linear_bwd_dw(dY, X)
-    assert_close(to_f64(got[which]), want, S, what=which + " (persistent grid)")
+    assert_close(to_f64(got[out]), want, S, what=which + " (persistent grid)")
 
 
 def test_persistent_grid_bitwise_at_8192_cubed():
