@@ -105,7 +105,8 @@ struct GemmParams {
   float* colsum;
   float* colsum_part;
   // DMA kernels, plain products of whole 256x256 tiles (no batch, split,
-  // column sums, activation or accumulation, M and N multiples of 256):
+  // activation or accumulation, M and N multiples of 256; column sums of A
+  // allowed):
   // the size of a persistent grid (one block per CU, each walking the tiles
   // of the plain grid's blocks b, b + persist, ...); 0: the plain grid
   int32_t persist;

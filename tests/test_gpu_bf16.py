@@ -184,7 +184,7 @@ def test_bf16_db_folded_into_dw(cfg, splits):
 
 def _three_products(inp):
     """Y, dX and dW as three calls (dW without db, so that no column sum
-    rides on it)."""
+    rides on it), then dW with db (the column sum of dY inside the product)."""
     x, w, bias, dy = (inp[k].to(DEV) for k in ("X", "W", "b", "dY"))
     M, K = x.shape
     N = w.shape[0]
@@ -194,8 +194,11 @@ def _three_products(inp):
     b.linear_fwd(x, w, bias, y)
     b.linear_bwd(x, w, dy, dx, None, None)
     b.linear_bwd(x, w, dy, None, dw, None)
+    dw2 = torch.full((N, K), float("nan"), device=DEV)
+    db = torch.full((N,), float("nan"), device=DEV)
+    b.linear_bwd(x, w, dy, None, dw2, db)
     torch.cuda.synchronize()
-    return {"Y": y, "dX": dx, "dW": dw}
+    return {"Y": y, "dX": dx, "dW": dw, "dW+db": dw2, "db": db}
 
 
 def _persist_on_off(inp):
@@ -233,7 +236,7 @@ def test_bf16_persistent_grid(cfg, which):
         got, plain = _persist_on_off(inp)
     finally:
         b.debug_set("cfg", -1)
-    for k in ("Y", "dX", "dW"):
+    for k in got:
         assert torch.equal(got[k], plain[k]), k
     X, W, B, dY = (to_f64(inp[k]) for k in ("X", "W", "b", "dY"))
     out = which.rstrip("1")
@@ -244,12 +247,15 @@ def test_bf16_persistent_grid(cfg, which):
     else:
         want, S = oracle.linear_bwd_dw(dY, X)
     check_bf16(to_f64(got[out]), want, S, which + " (persistent grid)")
+    if out == "dW":
+        assert torch.equal(got["dW+db"], got["dW"])
+        check_bf16(to_f64(got["db"]), *oracle.linear_bwd_db(dY), which + " db (persistent grid)")
 
 
 def test_bf16_persistent_grid_bitwise_at_16384x8192x8192():
     """The bench's products on the persistent grid (2048 tiles, eight per
     block) equal the plain grid's bit for bit."""
     got, plain = _persist_on_off(wl.LINEAR_16384x8192x8192_BF16.make())
-    for k in ("Y", "dX", "dW"):
+    for k in got:
         assert not torch.isnan(got[k]).any(), k
         assert torch.equal(got[k], plain[k]), k

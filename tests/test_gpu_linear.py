@@ -301,7 +301,7 @@ def test_linear_db_folded_into_dw(cfg, vec1, splits, shape):
 
 def _three_products(inp):
     """Y, dX and dW as three calls (dW without db, so that no column sum
-    rides on it)."""
+    rides on it), then dW with db (the column sum of dY inside the product)."""
     x, w, bias, dy = (inp[k].to(DEV) for k in ("X", "W", "b", "dY"))
     M, K = x.shape
     N = w.shape[0]
@@ -311,8 +311,11 @@ def _three_products(inp):
     b.linear_fwd(x, w, bias, y)
     b.linear_bwd(x, w, dy, dx, None, None)
     b.linear_bwd(x, w, dy, None, dw, None)
+    dw2 = torch.full((N, K), float("nan"), device=DEV)
+    db = torch.full((N,), float("nan"), device=DEV)
+    b.linear_bwd(x, w, dy, None, dw2, db)
     torch.cuda.synchronize()
-    return {"Y": y, "dX": dx, "dW": dw}
+    return {"Y": y, "dX": dx, "dW": dw, "dW+db": dw2, "db": db}
 
 
 def _persist_on_off(inp):
@@ -329,7 +332,9 @@ def _persist_on_off(inp):
 # (M, N, K) with 17 x 16 = 272 whole output tiles of 256x256 (more than the
 # CUs) for one product each: the forward (Y is M x N, with the bias), dX
 # (M x K) and dW (N x K); six K-stages of 32 in the product that is
-# persistent, or one (the loaders move to the next tile at every stage)
+# persistent, or one (the loaders move to the next tile at every stage).
+# fp32 dW stays on the plain grid (the persistent one measured slower), so
+# its case checks the plain grid against itself and the oracle
 PERSIST_SHAPES = {"Y": (4352, 4096, 192), "dX": (4352, 192, 4096), "dW": (192, 4352, 4096),
                   "Y1": (4352, 4096, 32), "dX1": (4352, 32, 4096)}
 
@@ -348,7 +353,7 @@ def test_persistent_grid(cfg, which):
         got, plain = _persist_on_off(inp)
     finally:
         b.debug_set("cfg", -1)
-    for k in ("Y", "dX", "dW"):
+    for k in got:
         assert torch.equal(got[k], plain[k]), k
     X, W, B, dY = (to_f64(inp[k]) for k in ("X", "W", "b", "dY"))
     out = which.rstrip("1")
@@ -359,12 +364,15 @@ def test_persistent_grid(cfg, which):
     else:
         want, S = oracle.linear_bwd_dw(dY, X)
     assert_close(to_f64(got[out]), want, S, what=which + " (persistent grid)")
+    if out == "dW":
+        assert torch.equal(got["dW+db"], got["dW"])
+        assert_close(to_f64(got["db"]), *oracle.linear_bwd_db(dY), what=which + " db (persistent grid)")
 
 
 def test_persistent_grid_bitwise_at_8192_cubed():
     """The bench's products on the persistent grid (1024 tiles, four per
     block) equal the plain grid's bit for bit."""
     got, plain = _persist_on_off(wl.LINEAR_8192x8192x8192_F32.make())
-    for k in ("Y", "dX", "dW"):
+    for k in got:
         assert not torch.isnan(got[k]).any(), k
         assert torch.equal(got[k], plain[k]), k
