@@ -428,13 +428,10 @@ mt_status launch_gemm(GemmCall& g, hipStream_t stream, void* ws, size_t ws_bytes
   if (e != hipSuccess) return hip_status(e);
   if (p.splits > 1) {
     // batch elements of C are contiguous M x N blocks when batched (mt_matmul)
+    // the column sums (unbatched products only) are added by the same finish
     e = mt::splitk_finish(p.partial, p.splits, p.keep_count * p.M, p.N, p.c, p.ldc, p.bias,
-                          p.accumulate != 0, stream);
+                          p.accumulate != 0, stream, p.colsum ? p.colsum_part : nullptr, p.colsum);
     if (e != hipSuccess) return hip_status(e);
-    if (p.colsum) {
-      e = mt::parts_finish(p.colsum_part, p.splits, p.M, p.colsum, p.accumulate != 0, stream);
-      if (e != hipSuccess) return hip_status(e);
-    }
   }
   return MT_OK;
 }

@@ -64,8 +64,12 @@ hipError_t gemm_bf16(const GemmParams& p, bool a_kc, bool b_kc, bool vec, int cf
                      hipStream_t stream);
 
 // Split-K finish: C[m][n] (+)= sum_s partial[s][m][n] (+ bias[n]), s ascending.
+// With cs_part (the runs' column sums of A, splits x M floats), also
+// cs_out[m] (+)= sum_s cs_part[s][m], s ascending (in the same launch where
+// the 16-byte form runs).
 hipError_t splitk_finish(const float* partial, int splits, int64_t M, int64_t N, float* c,
-                         int64_t ldc, const float* bias, bool accumulate, hipStream_t stream);
+                         int64_t ldc, const float* bias, bool accumulate, hipStream_t stream,
+                         const float* cs_part = nullptr, float* cs_out = nullptr);
 
 // Column sums over the outer axis of a row-major [M][N] matrix with row pitch
 // ld: out[n] (+)= sum_m x[m][n]. x is f32 or bf16 (is_bf16). With ws (room for

@@ -130,10 +130,21 @@ __global__ __launch_bounds__(256) void splitk_finish_kernel(const float* partial
 // The same sums four columns a lane with 16-byte accesses (N, ldc and every
 // base a multiple of 4 floats): blockIdx.x covers 1024 columns, blockIdx.y
 // strides over the rows. Each element is summed in the same order as above.
+// With cs_part, one more column of blocks adds the runs' column sums of A
+// (M of them) in run order, as parts_finish_kernel does, saving its launch.
 __global__ __launch_bounds__(256) void splitk_finish4_kernel(const float* partial, int splits,
                                                              int64_t M, int64_t N, float* c,
                                                              int64_t ldc, const float* bias,
-                                                             int accumulate) {
+                                                             int accumulate, const float* cs_part,
+                                                             float* cs_out) {
+  if (cs_part && blockIdx.x == gridDim.x - 1) {
+    const int64_t k = (int64_t)blockIdx.y * 256 + threadIdx.x;
+    if (k >= M) return;
+    float s = 0.f;
+    for (int q = 0; q < splits; ++q) s += cs_part[(int64_t)q * M + k];
+    cs_out[k] = accumulate ? cs_out[k] + s : s;
+    return;
+  }
   const int64_t n = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
   if (n >= N) return;
   const int64_t MN = M * N;
@@ -313,19 +324,28 @@ hipError_t reduce_strided(const float* x, const ReducePlan& plan, float* out, bo
 }
 
 hipError_t splitk_finish(const float* partial, int splits, int64_t M, int64_t N, float* c,
-                         int64_t ldc, const float* bias, bool accumulate, hipStream_t stream) {
+                         int64_t ldc, const float* bias, bool accumulate, hipStream_t stream,
+                         const float* cs_part, float* cs_out) {
   const int64_t n = M * N;
   if (n <= 0) return hipSuccess;
   auto a16 = [](const void* q) { return ((uintptr_t)q & 15) == 0; };
   if (N % 4 == 0 && ldc % 4 == 0 && a16(partial) && a16(c) && (!bias || a16(bias))) {
     const int64_t rows = M < 65535 ? M : 65535;
-    hipLaunchKernelGGL(splitk_finish4_kernel, dim3((unsigned)((N / 4 + 255) / 256), (unsigned)rows),
-                       dim3(256), 0, stream, partial, splits, M, N, c, ldc, bias, (int)accumulate);
-    return hipGetLastError();
+    // the column sums' blocks (one per 256 of them) fit in the grid's rows
+    const bool fold = cs_part && cs_out && (M + 255) / 256 <= rows;
+    hipLaunchKernelGGL(splitk_finish4_kernel,
+                       dim3((unsigned)((N / 4 + 255) / 256 + (fold ? 1 : 0)), (unsigned)rows), dim3(256),
+                       0, stream, partial, splits, M, N, c, ldc, bias, (int)accumulate,
+                       fold ? cs_part : nullptr, fold ? cs_out : nullptr);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || fold || !cs_part) return e;
+    return parts_finish(cs_part, splits, M, cs_out, accumulate, stream);
   }
   hipLaunchKernelGGL(splitk_finish_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream,
                      partial, splits, M, N, c, ldc, bias, (int)accumulate);
-  return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !cs_part) return e;
+  return parts_finish(cs_part, splits, M, cs_out, accumulate, stream);
 }
 
 hipError_t parts_finish(const float* ws, int parts, int64_t N, float* out, bool accumulate,
