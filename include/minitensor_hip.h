@@ -391,7 +391,8 @@ mt_status mt_matmul_shape(int32_t na, const int64_t* a, int32_t nb, const int64_
  * on their XCD and wrap around; 0 = every block starts at k = 0); "persist"
  * (1 = the default: plain products of whole 256x256 tiles, more tiles
  * than CUs, no accumulate, run on a grid of one block per CU that walks the
- * plain grid's tiles; 0 = the plain grid; the two give identical bits);
+ * plain grid's tiles, bf16 dW with db's column sums included, fp32 dW never;
+ * 0 = the plain grid; the two give identical bits);
  * convolution: "conv_gather" (1 = the default: products gather the image
  * where the layout allows; 0 = always unfold), "stream_k" (gathered 256x256
  * forward and input-gradient products: 0 never, 1 = the default: when the
