@@ -151,6 +151,10 @@ def test_conv2d_large_sampled():
     case = (32, 256, 56, 56, 256, 3, 3, (1, 1), (1, 1), "cl", "cl")
     x, w, bias, dy = make(case, seed=21)
     y, dx, dw, db = run(case, x, w, bias, dy)
+    # every element written (the outputs start as NaN): tiles computed whole
+    # and tiles summed from stream-K segments
+    for t, name in ((y, "y"), (dx, "dx"), (dw, "dw")):
+        assert not torch.isnan(t).any(), name
     X, Wt, B, dY = (to_f64(t) for t in (x, w, bias, dy))
     rng = np.random.default_rng(0)
     st, pd = case[7], case[8]
@@ -316,13 +320,14 @@ SK_CASES = [
 ]
 
 
-@pytest.mark.parametrize("blocks", [7, 13, 64])
+@pytest.mark.parametrize("blocks", [3, 5, 7, 13, 64])
 @pytest.mark.parametrize("case", SK_CASES, ids=[f"s{i}" for i in range(len(SK_CASES))])
 def test_conv2d_stream_k(case, blocks):
     """The gathered forward and input-gradient products in stream-K order over
     a forced number of blocks (tiles cut into 1-3 segments at arbitrary
-    stages, several tile rows and columns): against the oracle, and
-    bit-identical on a rerun (segments are summed in a fixed order)."""
+    stages, several tile rows and columns, up to three tiles' stages per
+    block): against the oracle, and bit-identical on a rerun (segments are
+    summed in a fixed order)."""
     x, w, bias, dy = make(case, seed=53)
     try:
         b.debug_set("cfg", 6)
