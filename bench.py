@@ -60,7 +60,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=-1,
-                    help="untimed warm-up steps (default: as many as take about a second, at "
+                    help="untimed warm-up steps (default: as many as take about three seconds, at "
                          "least 5, so that the GPU clock has ramped up before timing starts)")
     ap.add_argument("--workload", default="linear_8192x8192x8192_f32")
     ap.add_argument("--graph", action="store_true",
@@ -182,7 +182,8 @@ def timed_steps(step, n_events: int, steps: int, warmup: int):
     event at every step boundary (and events between a step's calls when
     n_events > 1). Returns (median ms per step, mean ms between each step's
     events, mean ms per step). warmup < 0: steps, each waited for, until
-    about a second has passed (at least 5)."""
+    about three seconds have passed (at least 5): the clock settles, and the
+    run holds the GPU busy long enough for an outside sampler to see it."""
     import statistics
 
     import torch
@@ -190,7 +191,7 @@ def timed_steps(step, n_events: int, steps: int, warmup: int):
     if warmup < 0:
         t = time.perf_counter()
         warmup = 0
-        while warmup < 5 or (time.perf_counter() - t < 1.0 and warmup < 100000):
+        while warmup < 5 or (time.perf_counter() - t < 3.0 and warmup < 100000):
             step()
             torch.cuda.synchronize()
             warmup += 1
