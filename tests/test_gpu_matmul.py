@@ -199,3 +199,37 @@ def test_reduce_broadcast_grad(oshape, ishape, layout, parts):
         b.debug_set("parts", 0)
     want, S = oracle.reduce_broadcast(g.double().numpy(), ishape)
     assert_close(to_f64(gi), want, S, what=f"{oshape}->{ishape}")
+
+
+@pytest.mark.parametrize("cfg", [6, 8, 9, 10, 13, 14, 15])
+@pytest.mark.parametrize("acc", [False, True])
+@pytest.mark.parametrize("layout", ["nn", "tn", "nt"])
+def test_bmm_odd_pitch_staged_epilogue(cfg, acc, layout):
+    """Odd pitches run on the DMA tiles with 4-byte lanes and stage their
+    output rows through LDS. Whole 32-row slabs take the straight-line store
+    path (columns past N dropped by the buffer stores); slabs cut by the last
+    row, and every accumulating product, take the per-row loop. C (+)= A B
+    against the oracle, in each operand layout (tn: A an M-contiguous view;
+    nt: B a K-contiguous view), on every DMA tile that serves odd pitches."""
+    if cfg == 14 and layout != "nt":
+        pytest.skip("the 256x96 tile takes a K-contiguous B only")
+    M, K, N = 301, 67, 389
+    if layout == "tn":
+        A = wl.tensor((2, 1, K, M), ("uniform", 1.0), seed=11).transpose(-1, -2)
+    else:
+        A = wl.tensor((2, 1, M, K), ("uniform", 1.0), seed=11)
+    if layout == "nt":
+        B = wl.tensor((1, 3, N, K), ("uniform", 1.0), seed=12).transpose(-1, -2)
+    else:
+        B = wl.tensor((1, 3, K, N), ("uniform", 1.0), seed=12)
+    prior = torch.randn(2, 3, M, N) if acc else None
+    b.debug_set("cfg", cfg)
+    try:
+        C = gpu_matmul(A.to(DEV), (2, 3, M, N), B.to(DEV), accumulate=acc,
+                       prior=prior.to(DEV) if acc else None)
+    finally:
+        b.debug_set("cfg", -1)
+    Cr, SC = oracle.matmul(A.double().numpy(), B.double().numpy())
+    if acc:
+        Cr, SC = Cr + prior.double().numpy(), SC + 1
+    assert_close(to_f64(C), Cr, SC, what=f"C{'+' if acc else ''}= cfg {cfg} {layout}")
