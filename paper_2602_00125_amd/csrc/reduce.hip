@@ -130,6 +130,41 @@ __global__ __launch_bounds__(256) void splitk_finish_kernel(const float* partial
   *dst = accumulate ? *dst + s : s;
 }
 
+// The element sums above, four consecutive elements of the flattened M x N
+// partial a lane (M N a multiple of 4 and the partial 16-byte aligned, so
+// every run's slice is): one 16-byte load per run instead of four 4-byte
+// ones, the stores one element at a time along C's rows (odd pitches). Each
+// element is summed in the same order as above.
+__global__ __launch_bounds__(256) void splitk_finish_flat4_kernel(const float* partial, int splits,
+                                                                  int64_t M, int64_t N, float* c,
+                                                                  int64_t ldc, const float* bias,
+                                                                  int accumulate) {
+  const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  const int64_t MN = M * N;
+  if (i >= MN) return;
+  float4 s = {0.f, 0.f, 0.f, 0.f};
+  for (int p = 0; p < splits; ++p) {
+    const float4 v = *(const float4*)(partial + (int64_t)p * MN + i);
+    s.x += v.x;
+    s.y += v.y;
+    s.z += v.z;
+    s.w += v.w;
+  }
+  int64_t m = i / N, n = i - m * N;
+  const float e[4] = {s.x, s.y, s.z, s.w};
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    float x = e[u];
+    if (bias) x += bias[n];
+    float* dst = c + m * ldc + n;
+    *dst = accumulate ? *dst + x : x;
+    if (++n == N) {
+      n = 0;
+      ++m;
+    }
+  }
+}
+
 // The same sums four columns a lane with 16-byte accesses (N, ldc and every
 // base a multiple of 4 floats): blockIdx.x covers 1024 columns, blockIdx.y
 // strides over the rows. Each element is summed in the same order as above.
@@ -344,8 +379,12 @@ hipError_t splitk_finish(const float* partial, int splits, int64_t M, int64_t N,
     if (e != hipSuccess || fold || !cs_part) return e;
     return parts_finish(cs_part, splits, M, cs_out, accumulate, stream);
   }
-  hipLaunchKernelGGL(splitk_finish_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream,
-                     partial, splits, M, N, c, ldc, bias, (int)accumulate);
+  if (n % 4 == 0 && a16(partial))
+    hipLaunchKernelGGL(splitk_finish_flat4_kernel, dim3((unsigned)((n / 4 + 255) / 256)), dim3(256), 0,
+                       stream, partial, splits, M, N, c, ldc, bias, (int)accumulate);
+  else
+    hipLaunchKernelGGL(splitk_finish_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream,
+                       partial, splits, M, N, c, ldc, bias, (int)accumulate);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !cs_part) return e;
   return parts_finish(cs_part, splits, M, cs_out, accumulate, stream);
