@@ -166,18 +166,35 @@ static hipError_t conv_cfg(const GemmParams& p, int cfg, hipStream_t stream) {
 
 // Sum of the segments of every tile the stream-K product cut: C = sum over
 // slots s < n(t) of partial[s] (+ bias, + C), slots in order; tiles computed
-// whole were written by the product. A lane per 4 consecutive columns.
-__global__ __launch_bounds__(256) void sk_finish_kernel(const GemmParams p, int64_t G, int BM,
-                                                        int BN) {
+// whole were written by the product. A lane per 4 consecutive columns. The
+// lane's row and its tile's segment count take integer divisions; where the
+// sizes allow (NARROW: M N / 4 and the stage count times G below 2^32) they
+// are 32-bit ones, a fraction of the instructions of 64-bit division.
+template <int BM, int BN, bool NARROW>
+__global__ __launch_bounds__(256) void sk_finish_kernel(const GemmParams p, int64_t G) {
   typedef float f32x4 __attribute__((ext_vector_type(4)));
   const int64_t n4 = p.N / 4;
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= p.M * n4) return;
-  const int64_t m = i / n4, n = (i - m * n4) * 4;
   const int64_t ks = (p.K + 31) / 32;
   const int64_t U = (int64_t)p.tiles_m * p.tiles_n * ks;
-  const int64_t t = (m / BM) * p.tiles_n + n / BN;
-  const gemm::SkSeg sg = gemm::sk_segment(t, 0, ks, G, U);
+  int64_t m, n;
+  gemm::SkSeg sg;
+  if constexpr (NARROW) {
+    const uint32_t q = (uint32_t)i / (uint32_t)n4;
+    m = q;
+    n = ((uint32_t)i - q * (uint32_t)n4) * 4;
+    const uint32_t t = (uint32_t)(m / BM) * (uint32_t)p.tiles_n + (uint32_t)(n / BN);
+    const uint32_t g = (uint32_t)G, u = (uint32_t)U, L = t * (uint32_t)ks;
+    // sk_count(X) = ceil(X G / U) in 32 bits (X G <= U G < 2^32)
+    auto cnt = [&](uint32_t X) { return (X * g + u - 1) / u; };
+    sg.n = (int)(cnt(L + (uint32_t)ks) - cnt(L + 1) + 1);
+  } else {
+    m = i / n4;
+    n = (i - m * n4) * 4;
+    const int64_t t = (m / BM) * p.tiles_n + n / BN;
+    sg = gemm::sk_segment(t, 0, ks, G, U);
+  }
   if (sg.n <= 1) return;
   const float* src = p.partial + m * p.N + n;
   f32x4 v = *(const f32x4*)src;
@@ -209,8 +226,12 @@ hipError_t gemm_f32_conv_sk(const GemmParams& p, int mode, int blocks, hipStream
   if (e != hipSuccess) return e;
   const int64_t groups = p.M * (p.N / 4);
   if ((groups + 255) / 256 > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL(sk_finish_kernel, dim3((unsigned)((groups + 255) / 256)), dim3(256), 0, stream,
-                     q, (int64_t)blocks, 256, 256);
+  const int64_t units = (int64_t)q.tiles_m * q.tiles_n * (p.K / 32);
+  const dim3 grid((unsigned)((groups + 255) / 256));
+  if (groups < (int64_t(1) << 32) && units * blocks + units < (int64_t(1) << 32))
+    hipLaunchKernelGGL((sk_finish_kernel<256, 256, true>), grid, dim3(256), 0, stream, q, (int64_t)blocks);
+  else
+    hipLaunchKernelGGL((sk_finish_kernel<256, 256, false>), grid, dim3(256), 0, stream, q, (int64_t)blocks);
   return hipGetLastError();
 }
 
