@@ -332,8 +332,9 @@ size_t plan_gemm(GemmCall& g, bool may_split) {
       g.cfg = mt::kCfg128x128;
     }
   }
-  // the column sums of A fold into the DMA kernels of plain TN products only
-  if (p.colsum && (g.a_kc || g.conv || p.nred > 0 || p.keep_count != 1 ||
+  // the column sums of A fold into the DMA kernels of plain TN products and
+  // of the convolution's weight gradient only
+  if (p.colsum && (g.a_kc || (g.conv && g.conv != 2) || p.nred > 0 || p.keep_count != 1 ||
                    !dma_kernel(g.cfg, g.vec, g.bf16)))
     p.colsum = nullptr;
   p.colsum_part = nullptr;

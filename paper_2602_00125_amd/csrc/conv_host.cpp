@@ -330,6 +330,7 @@ mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
   // few output tiles under-fill the GPU; partial tiles go after U
   GemmCall gdw{};
   size_t need_dw = 0;
+  bool fold_db = false;
   if (dw) {
     init_params(&gdw.p);
     gdw.p.a = dy->data;
@@ -353,15 +354,19 @@ mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
       gdw.p.b = x->data;
       gdw.p.ldb = 0;
     }
+    // db = the column sums of dY^T, A of this product: folded into it where
+    // its kernel allows (no second pass over dY); the plan settles whether
+    gdw.p.colsum = db ? (float*)db->data : nullptr;
     GemmCall probe = gdw;
     need_dw = plan_gemm(probe, true);
+    fold_db = probe.p.colsum != nullptr;
   }
   int parts = 1;
   size_t need_db = 0;
   if (db && cp.M > 0) {
     const int fp = g_force_parts;
     parts = fp > 0 ? fp : mt::colsum_parts(cp.M, g.CO);
-    if (parts > 1) need_db = (size_t)parts * g.CO * sizeof(float);
+    if (parts > 1 && !fold_db) need_db = (size_t)parts * g.CO * sizeof(float);
   }
   // dx = V W in one product where dy can be gathered (V: dy over the
   // mirrored taps), its rows the input pixels
@@ -425,7 +430,10 @@ mt_status conv_bwd_impl(const mt_tensor* x, const mt_tensor* w, const mt_tensor*
   } else if (dw) {
     if ((s = launch_gemm(gdw, stream, rest_bytes ? rest : nullptr, rest_bytes))) return s;
   }
-  if (db) {
+  // the product summed db itself (it ran: dW is not empty, and its kernel
+  // kept the column sums)
+  fold_db = dw && gdw.p.colsum != nullptr && gdw.p.M > 0 && gdw.p.N > 0;
+  if (db && !fold_db) {
     (void)hipGetLastError();
     float* wsp = (rest && parts > 1 && rest_bytes >= need_db) ? (float*)rest : nullptr;
     if ((s = hip_status(mt::colsum(dy->data, false, cp.M, g.CO, g.CO, (float*)db->data, acc, wsp,
