@@ -285,7 +285,9 @@ mt_status mt_conv2d_fwd_workspace(const mt_tensor* x, const mt_tensor* w, const 
  *   channels-last or [N][C][H][W]; dw the shape of w with its taps in w's
  *   order; db [CO]. x and w are needed for their shapes (and x's data for
  *   dw, w's data for dx). flags: MT_ACCUMULATE, MT_CONV_REUSE_UNFOLD. The input gradient is a
- *   gather over the taps that read each element: no atomics, deterministic.
+ *   gather over the taps that read each element: no atomics, deterministic. With dw and db
+ *   both requested, db is summed inside the dW product (the column sums of dY^T, its first
+ *   operand); db alone runs a column-sum pass over dy.
  */
 mt_status mt_conv2d_bwd(const mt_tensor* x, const mt_tensor* w, const mt_tensor* dy,
                         const mt_tensor* dx, const mt_tensor* dw, const mt_tensor* db,
