@@ -259,6 +259,28 @@ def test_conv2d_gather_split_weight_gradient():
     check(case, x, w, bias, dy, *got)
 
 
+@pytest.mark.parametrize("co", [32, 44])
+@pytest.mark.parametrize("splits", [0, 3, 5])
+@pytest.mark.parametrize("acc", [False, True])
+def test_conv2d_db_inside_weight_gradient(co, splits, acc):
+    """db summed inside the gathered dW product (the column sums of dY^T, its
+    first operand): whole or split into runs whose parts the finish adds,
+    with and without accumulation, an output-channel count that leaves part
+    of a tile, against the oracle."""
+    case = (7, 32, 30, 29, co, 3, 3, (1, 1), (1, 1), "cl", "cl")
+    x, w, bias, dy = make(case, seed=41)
+    prior = None
+    if acc:
+        prior = (None, wl.tensor((co, 32, 3, 3), ("normal",), seed=43).to(DEV),
+                 wl.tensor((co,), ("normal",), seed=44).to(DEV))
+    try:
+        b.debug_set("splits", splits)
+        got = run(case, x, w, bias, dy, outputs=("dw", "db"), accumulate=acc, prior=prior)
+    finally:
+        b.debug_set("splits", 0)
+    check(case, x, w, bias, dy, *got, prior=prior)
+
+
 def test_conv2d_reuse_flag_after_a_gathering_forward():
     """The forward gathered (no unfolded input left in the workspace) and the
     weight gradient cannot (dw 4 bytes off 16-byte alignment): the backward
